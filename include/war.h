@@ -1,0 +1,198 @@
+/*
+ * war.h -- C ABI of the MI355X speculative-verification decode step.
+ *
+ * The operation (WAR, arXiv 2607.17299):
+ *  - Rollout is batched LLM inference over multi-turn trajectories whose KV
+ *    cache is kept and reused from turn to turn (Background, "Rollout
+ *    Bottlenecks"; System Design, "Overview of WAR").
+ *  - Under low load the model-free suffix drafter proposes draft tokens.  The
+ *    target model verifies them in one forward pass and advances several tokens
+ *    when they are accepted (System Design, "SuffixDecoding").
+ *  - Under high load speculation is off and the same step is plain batched
+ *    decode (System Design, "SuffixDecoding": adaptive enabling, stateless
+ *    mode switching).
+ *  - Speculation must be lossless (Introduction; Background, "Why Workload
+ *    Matters").  Here that means greedy verification:
+ *      - row 0 of request b is its pending token x_b at position ctx_b;
+ *      - rows 1..n_b are its drafts d_1..d_n;
+ *      - g_i is the argmax of row i (ties go to the lowest id);
+ *      - accept_b is the largest a with d_m == g_{m-1} for all m <= a;
+ *      - next_b is g_{accept_b}.
+ *    war_kv_commit then keeps the KV of rows 0..accept_b, sets
+ *    ctx_b += accept_b + 1, and returns the pages reserved for rejected
+ *    slots (rollback).
+ *
+ * Conventions
+ *  - Every array argument is a DEVICE pointer owned by the caller, unless its
+ *    comment says "host".  The library never frees caller memory.
+ *  - Every call is ordered on the given HIP stream (a hipStream_t passed as
+ *    void*; NULL = the null stream).  Nothing waits for the device unless the
+ *    comment says so.
+ *  - Calls on one model or one pool are not thread-safe: use one stream per
+ *    model and pool.
+ *  - Arguments are checked on the host before anything is enqueued.  On error
+ *    the call returns a negative status, enqueues nothing and changes no
+ *    state.  war_last_error() describes the last failure of the calling
+ *    thread.
+ */
+#ifndef WAR_H
+#define WAR_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t war_status;
+#define WAR_OK                0
+#define WAR_ERR_INVALID_ARG  (-1)
+#define WAR_ERR_OUT_OF_PAGES (-2)
+#define WAR_ERR_HIP          (-3)
+#define WAR_ERR_UNSUPPORTED  (-4)
+#define WAR_ERR_DEVICE       (-5) /* the device flagged bad input (war_pool_check) */
+
+/* Decoder shape.
+ * Layers: RMSNorm -> QKV -> rotate-half RoPE -> grouped-query attention -> O-proj,
+ * then residual -> RMSNorm -> SwiGLU FFN -> residual; final RMSNorm; untied LM head.
+ * Constraints: d_model, ffn_dim, vocab and (n_q_heads + 2 n_kv_heads) * head_dim
+ * are multiples of 128; head_dim is 64 or 128; n_q_heads / n_kv_heads is 1..8;
+ * page_size is 16. */
+typedef struct war_model_config {
+  int32_t n_layers, d_model, n_q_heads, n_kv_heads, head_dim, ffn_dim, vocab;
+  float rms_eps;     /* RMSNorm epsilon                                        */
+  float rope_base;   /* RoPE base: pair j of a head turns by pos * base^(-2j/D) */
+  int32_t page_size; /* KV tokens per page (16)                                */
+  int32_t max_rows;  /* most rows one forward pass holds (verify: B*(k_max+1)) */
+} war_model_config;
+
+typedef struct war_model war_model;     /* opaque: borrowed weights + owned workspace */
+typedef struct war_kv_pool war_kv_pool; /* opaque: owned allocator state, borrowed KV */
+
+/* Number of weight pointers a model takes: 3 + 7 * n_layers. */
+int32_t war_weight_count(const war_model_config* cfg);
+
+/* Create a model over caller-owned bf16 weights (device pointers, row-major [out, in]).
+ * Canonical order:
+ *   embed [V, d];
+ *   then for each layer:
+ *     attn_norm [d];
+ *     w_qkv [(nq + 2 nkv) * hd, d]  (query rows head-major, then key rows, then value rows);
+ *     w_o [d, nq * hd];
+ *     ffn_norm [d];
+ *     w_gate [F, d];
+ *     w_up [F, d];
+ *     w_down [d, F];
+ *   then final_norm [d];
+ *   then w_lm [V, d].
+ * The model borrows the pointers: they must outlive it.  It allocates its own
+ * device workspace (sized by max_rows).  Returns WAR_ERR_UNSUPPORTED for shapes
+ * outside the constraints above. */
+war_status war_model_create(const war_model_config* cfg, const void* const* weights,
+                            int32_t n_weights, war_model** out);
+void war_model_destroy(war_model* m);
+
+/* Create a KV page pool over caller-owned storage.
+ *   kv_pages     bf16, n_layers * num_pages * n_kv_heads * 2 * page_size * head_dim
+ *                elements.  Page p of layer l, kv-head h starts at element
+ *                ((l * num_pages + p) * n_kv_heads + h) * 2 * page_size * head_dim.
+ *                It holds the keys as [page_size][head_dim], then the values
+ *                transposed as [head_dim][page_size].
+ *   block_tables int32 [max_seqs][max_pages_per_seq].  Entry [s][j] is the
+ *                physical page of sequence s's logical page j, or -1.
+ *                Initialised to -1 here.
+ * The pool owns its free stack, reference counts and per-sequence page counts.
+ * Free pages pop as 0, 1, 2, ...  Pops go in batch order, logical pages
+ * ascending.  Pushes go in reverse batch order, logical pages descending.  So
+ * reserving and then discarding a step restores the stack exactly. */
+war_status war_kv_pool_create(const war_model_config* cfg, void* kv_pages, int32_t num_pages,
+                              int32_t* block_tables, int32_t max_seqs, int32_t max_pages_per_seq,
+                              void* stream, war_kv_pool** out);
+void war_kv_pool_destroy(war_kv_pool* p);
+
+/* Ensure capacity for n_tokens[i] slots for sequence seq_ids[i] (host arrays, distinct ids). */
+war_status war_kv_alloc(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host,
+                        const int32_t* n_tokens_host, void* stream);
+
+/* dst shares the first n_tokens (a multiple of page_size) of src.  dst must hold no
+ * pages.  The shared pages' reference counts rise.  The caller sets dst's
+ * ctx_len to n_tokens.  Cache reuse across sibling rollouts (System Design,
+ * "Overview of WAR"). */
+war_status war_kv_fork(war_kv_pool* p, int32_t src_seq, int32_t dst_seq, int32_t n_tokens,
+                       void* stream);
+
+/* Drop every page of each listed sequence (host array, distinct ids); a page
+ * returns to the free stack when its reference count reaches 0. */
+war_status war_kv_free(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host, void* stream);
+
+/* Write precomputed keys/values of tokens [pos0, pos0 + n) of one layer of one
+ * sequence into its pages (capacity must already be there, e.g. war_kv_alloc).
+ * src: bf16 [2][n_kv_heads][n][head_dim] (0 = keys after RoPE, 1 = values).
+ * Imports a cached context computed elsewhere, such as another replica's. */
+war_status war_kv_load(war_kv_pool* p, int32_t seq_id, int32_t layer, int32_t pos0, int32_t n,
+                       const void* src, void* stream);
+
+/* Append a new turn to cached trajectories (System Design, "Overview of WAR";
+ * Background, "Rollout Bottlenecks").
+ *   seq_ids     device int32 [n]
+ *   ctx_lens    device int32 [n]; read, then += n_new
+ *   n_new_host  HOST int32 [n], >= 1
+ *   new_tokens  device int32, packed: sequence i's tokens at offset sum_{j<i} n_new[j]
+ *   next_tokens device int32 [n]: argmax after each sequence's last new token
+ *   last_logits device fp32 [n][vocab], or NULL
+ * Reserves pages for ctx + n_new slots and computes the new tokens' KV (causal,
+ * against the cached context).  This call synchronises the stream once to read
+ * ctx_lens. */
+war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int32_t* seq_ids,
+                              int32_t* ctx_lens, const int32_t* n_new_host,
+                              const int32_t* new_tokens, int32_t* next_tokens,
+                              float* last_logits, void* stream);
+
+/* One speculative-verification step over B requests (k_max = 0: plain decode).
+ *   seq_ids      device int32 [B], distinct
+ *   ctx_lens     device int32 [B]  cached tokens per request (not changed here)
+ *   last_tokens  device int32 [B]  pending token (previous step's next_tokens)
+ *   draft_tokens device int32 [B][k_max] (may be NULL when k_max == 0)
+ *   draft_lens   device int32 [B]  in [0, k_max] (NULL: all k_max)
+ *   accept_lens  device int32 [B]  out
+ *   next_tokens  device int32 [B]  out
+ *   logits       device fp32 [B * (k_max + 1)][vocab] or NULL.  Row b*(k_max+1)+i
+ *                holds request b's row i; rows with i > draft_len are unspecified.
+ * Reserves the pages for ctx + draft_len + 1 slots, writes the KV of all rows,
+ * and leaves the pool waiting for war_kv_commit.  Until that commit the pool
+ * accepts no other call that changes pages. */
+war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                           const int32_t* ctx_lens, const int32_t* last_tokens,
+                           const int32_t* draft_tokens, const int32_t* draft_lens, int32_t k_max,
+                           int32_t* accept_lens, int32_t* next_tokens, float* logits,
+                           void* stream);
+
+/* Commit the pending verify step.
+ *   accept_lens device int32 [B]; -1 discards the step.  Values are clamped
+ *               to [-1, reserved capacity].
+ * Effects:
+ *   ctx_lens[b] += accept_lens[b] + 1;
+ *   the pages the step reserved beyond the new length go back to the free
+ *   stack, and their block-table entries become -1.
+ * Use the same B, seq_ids and ctx_lens as the verify step. */
+war_status war_kv_commit(war_kv_pool* p, int32_t B, const int32_t* seq_ids, int32_t* ctx_lens,
+                         const int32_t* accept_lens, void* stream);
+
+/* Synchronise the stream.  Copy the allocator state to HOST buffers (each may
+ * be NULL):
+ *   free_stack      [num_pages]  (only the first *free_count entries are meaningful)
+ *   refcount        [num_pages]
+ *   held            [max_seqs]   pages held per sequence
+ *   step_base       [max_seqs]   pages held before the last reservation
+ * Returns WAR_ERR_DEVICE if a kernel flagged bad device-side input (a token
+ * id outside [0, vocab), or a device page shortage). */
+war_status war_pool_state(war_kv_pool* p, int32_t* free_count, int32_t* free_stack,
+                          int32_t* refcount, int32_t* held, int32_t* step_base, void* stream);
+
+/* Thread-local description of the last non-OK status ("" if none). */
+const char* war_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WAR_H */

@@ -1,0 +1,33 @@
+/*
+ * war_debug.h -- diagnostic entry points of libwar.so (not part of the verify path).
+ */
+#ifndef WAR_DEBUG_H
+#define WAR_DEBUG_H
+
+#include "war.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* One 16x16x32 bf16 matrix-core product C = A @ B with the lane layout the
+ * library's kernels assume.
+ *   A  device bf16 [16][32], row-major
+ *   B  device bf16 [32][16], row-major
+ *   C  device fp32 [16][16], row-major (out)
+ * Used by tests to confirm that layout on the hardware; stream-ordered. */
+war_status war_debug_mfma16(const void* A, const void* B, float* C, void* stream);
+
+/* Device address and size of one of a model's workspace buffers, for tests that
+ * inspect intermediate values after a call (the buffers hold the last layer's
+ * values).  Names: "h" fp32 residual [rows][d]; "u" bf16 last norm or SwiGLU
+ * output; "q" bf16 rotated queries [rows][nq*hd]; "o" bf16 attention output
+ * [rows][nq*hd]; "P" fp32 split-K partials; "pm", "pl", "po" attention
+ * partials; "rows", "reqs", "items" step metadata.  The pointer stays valid
+ * until the next call on the model. */
+war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* WAR_DEBUG_H */

@@ -1,0 +1,338 @@
+// Paged-KV bookkeeping kernels: free stack, reference counts, block tables,
+// reserve / commit / rollback / fork / free, and the verify-step setup that
+// reserves draft slots and builds the step's row metadata and attention work list.
+//
+// Every bookkeeping kernel runs as ONE workgroup of 1024 threads, so its effect
+// is a deterministic function of its inputs (no cross-workgroup atomics).
+// Policy: pops for batch entries in ascending order, logical pages ascending;
+// pushes in descending entry order, logical pages descending -- a reserve
+// followed by a discard restores the stack exactly.
+#include "kernels.h"
+
+namespace {
+
+constexpr int kBT = 1024;
+
+// Exclusive scan of one int per thread over the block; *total receives the sum.
+__device__ int block_excl_scan(int v, int* sh, int* total) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  int x = v;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  __syncthreads();
+  if (lane == 63) sh[w] = x;
+  __syncthreads();
+  int off = 0, tot = 0;
+  for (int i = 0; i < nw; ++i) {
+    if (i < w) off += sh[i];
+    tot += sh[i];
+  }
+  *total = tot;
+  __syncthreads();
+  return off + x - v;
+}
+
+__global__ void k_pool_init(PoolDev p) {
+  const int64_t n_tab = (int64_t)p.max_seqs * p.max_pages;
+  const int64_t n_all = n_tab > p.num_pages ? n_tab : (int64_t)p.num_pages;
+  for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n_all;
+       i += (int64_t)gridDim.x * blockDim.x) {
+    if (i < n_tab) p.table[i] = -1;
+    if (i < p.num_pages) {
+      p.stack[i] = p.num_pages - 1 - (int32_t)i;
+      p.refcount[i] = 0;
+    }
+    if (i < p.max_seqs) {
+      p.held[i] = 0;
+      p.base[i] = 0;
+    }
+    if (i == 0) {
+      p.scalars[0] = p.num_pages;
+      p.scalars[1] = 0;
+    }
+  }
+}
+
+// Pop `need` pages for entry (seq s) after `off` earlier pops of this call.
+__device__ void pop_pages(const PoolDev& p, int s, int need, int off, int fc) {
+  const int h = p.held[s];
+  int32_t* row = p.table + (int64_t)s * p.max_pages;
+  for (int j = 0; j < need; ++j) {
+    const int page = p.stack[fc - 1 - (off + j)];
+    row[h + j] = page;
+    p.refcount[page] = 1;
+  }
+}
+
+// Grow sequences to `target` pages (mode 0: alloc, targets from n_tokens;
+// mode 1: prefill, targets from ctx + n_new).  One thread per entry, n <= 1024.
+__global__ void __launch_bounds__(kBT) k_grow(PoolDev p, int n, const int32_t* seq_ids,
+                                              const int32_t* a, const int32_t* b, int mode) {
+  __shared__ int sh[16];
+  __shared__ int s_fail;
+  const int t = threadIdx.x;
+  int s = 0, need = 0, target = 0;
+  if (t < n) {
+    s = seq_ids[t];
+    const int tokens = mode == 0 ? a[t] : a[t] + b[t];
+    target = cdiv_i(tokens, p.page_size);
+    need = max(0, target - p.held[s]);
+  }
+  int total;
+  const int off = block_excl_scan(need, sh, &total);
+  const int fc = p.scalars[0];
+  if (t == 0) s_fail = total > fc;
+  __syncthreads();
+  if (s_fail) {
+    if (t == 0) p.scalars[1] |= ERR_NO_PAGES;
+    return;
+  }
+  if (t < n) {
+    pop_pages(p, s, need, off, fc);
+    p.held[s] += need;
+    p.base[s] = p.held[s];
+  }
+  __syncthreads();
+  if (t == 0) p.scalars[0] = fc - total;
+}
+
+// Verify-step setup: reserve pages for ctx + draft_len + 1 slots per request,
+// then build the padded row layout (row b*(k+1)+i = request b, token i) and the
+// attention work list (one item per `chunk` keys of each request).
+__global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs a, StepMeta m) {
+  __shared__ int sh[16];
+  __shared__ int s_fail;
+  __shared__ int s_ctx[kBT], s_dl[kBT];
+  const int t = threadIdx.x;
+  const int kp1 = a.k_max + 1;
+  __shared__ int s_bad;
+  if (t == 0) s_bad = 0;
+  __syncthreads();
+  int s = 0, need = 0, ctx = 0, dl = 0, hb = 0;
+  if (t < a.B) {
+    s = a.seq_ids[t];
+    ctx = a.ctx_lens[t];
+    dl = a.draft_lens ? a.draft_lens[t] : a.k_max;
+    dl = min(max(dl, 0), a.k_max);
+    // a bad id, a negative length or a request beyond its block-table row
+    // fails the whole step (no page moves, no row is active)
+    if (s < 0 || s >= p.max_seqs || ctx < 0 ||
+        cdiv_i(ctx + dl + 1, p.page_size) > p.max_pages) {
+      s = 0;
+      ctx = 0;
+      atomicOr(&s_bad, 1);
+    } else {
+      hb = p.held[s];
+      need = max(0, cdiv_i(ctx + dl + 1, p.page_size) - hb);
+    }
+  }
+  int total;
+  const int off = block_excl_scan(need, sh, &total);
+  const int fc = p.scalars[0];
+  if (t == 0) {
+    s_fail = total > fc || s_bad;
+    if (s_bad) atomicOr(&p.scalars[1], ERR_BAD_TOKEN);
+  }
+  __syncthreads();
+  const bool fail = s_fail;
+  if (t < a.B) {
+    if (!fail) {
+      pop_pages(p, s, need, off, fc);
+      p.held[s] = hb + need;
+      p.base[s] = hb;
+    }
+    s_ctx[t] = ctx;
+    s_dl[t] = fail ? -1 : dl;
+    m.req_seq[t] = s;
+    m.req_pos0[t] = ctx;
+    m.req_ntok[t] = fail ? 0 : dl + 1;
+    m.req_row0[t] = t * kp1;
+  }
+  // attention items: chunks of the keys visible to the request's last row
+  const int nch = (t < a.B && !fail) ? cdiv_i(ctx + dl + 1, a.chunk) : 0;
+  int n_items;
+  const int ioff = block_excl_scan(nch, sh, &n_items);
+  if (t < a.B) {
+    m.seg_begin[t] = ioff;
+    m.seg_count[t] = nch;
+    m.seg_req[t] = t;
+    m.seg_rb[t] = 0;
+    for (int c = 0; c < nch; ++c) m.items[ioff + c] = make_int4(t, 0, c, 0);
+  }
+  if (t == 0) {
+    m.n_items[0] = n_items;
+    if (fail && !s_bad) p.scalars[1] |= ERR_NO_PAGES;
+    if (!fail) p.scalars[0] = fc - total;
+  }
+  __syncthreads();
+  // rows: request b's token i sits in row b*(k_max+1)+i
+  const int R = a.B * kp1;
+  for (int r = t; r < R; r += blockDim.x) {
+    const int b = r / kp1, i = r % kp1;
+    const int dlb = s_dl[b];
+    const bool act = i <= dlb;
+    int tok = 0;
+    if (act) tok = i == 0 ? a.last_tokens[b] : a.draft_tokens[(int64_t)b * a.k_max + i - 1];
+    if (tok < 0 || tok >= a.vocab) {
+      atomicOr(&p.scalars[1], ERR_BAD_TOKEN);
+      tok = 0;
+    }
+    m.tok[r] = tok;
+    m.active[r] = act ? 1 : 0;
+    m.row_req[r] = b;
+    m.pos[r] = s_ctx[b] + min(i, max(dlb, 0));
+  }
+}
+
+// Commit: keep ctx + a + 1 tokens, push the step's pages beyond them
+// (entries in descending order, logical pages descending).
+__global__ void __launch_bounds__(kBT) k_commit(PoolDev p, int B, const int32_t* seq_ids,
+                                                int32_t* ctx_lens, const int32_t* accept) {
+  __shared__ int sh[16];
+  const int t = threadIdx.x;
+  const int rt = B - 1 - t;  // entry handled by this thread, so the scan runs descending
+  int s = 0, h = 0, keep = 0, rel = 0, new_ctx = 0;
+  if (t < B) {
+    s = seq_ids[rt];
+    h = p.held[s];
+    const int ctx = ctx_lens[rt];
+    const int cap = h * p.page_size;
+    const int acc = min(max(accept[rt], -1), cap - ctx - 1);
+    new_ctx = ctx + max(acc, -1) + 1;
+    keep = min(h, max(p.base[s], cdiv_i(new_ctx, p.page_size)));
+    rel = h - keep;
+  }
+  int total;
+  const int off = block_excl_scan(rel, sh, &total);
+  const int fc = p.scalars[0];
+  if (t < B) {
+    int32_t* row = p.table + (int64_t)s * p.max_pages;
+    for (int j = 0; j < rel; ++j) {
+      const int page = row[h - 1 - j];
+      p.stack[fc + off + j] = page;
+      p.refcount[page] -= 1;
+      row[h - 1 - j] = -1;
+    }
+    p.held[s] = keep;
+    p.base[s] = keep;
+    ctx_lens[rt] = new_ctx;
+  }
+  __syncthreads();
+  if (t == 0) p.scalars[0] = fc + total;
+}
+
+// Free sequences: entries in descending order; within one, logical pages
+// descending; a page is pushed when its count drops to 0.
+__global__ void __launch_bounds__(kBT) k_free(PoolDev p, int n, const int32_t* seq_ids) {
+  __shared__ int sh[16];
+  __shared__ int s_fc;
+  if (threadIdx.x == 0) s_fc = p.scalars[0];
+  __syncthreads();
+  for (int e = n - 1; e >= 0; --e) {
+    const int s = seq_ids[e];
+    const int h = p.held[s];
+    int32_t* row = p.table + (int64_t)s * p.max_pages;
+    for (int c0 = 0; c0 < h; c0 += blockDim.x) {
+      const int j = h - 1 - (c0 + threadIdx.x);  // descending logical page
+      int page = -1, push = 0;
+      if (j >= 0) {
+        page = row[j];
+        push = p.refcount[page] == 1;
+      }
+      int total;
+      const int off = block_excl_scan(push, sh, &total);
+      const int fc = s_fc;
+      if (j >= 0) {
+        p.refcount[page] -= 1;
+        if (push) p.stack[fc + off] = page;
+        row[j] = -1;
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) s_fc = fc + total;
+      __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+      p.held[s] = 0;
+      p.base[s] = 0;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) p.scalars[0] = s_fc;
+}
+
+__global__ void k_fork(PoolDev p, int src, int dst, int npg) {
+  const int32_t* rs = p.table + (int64_t)src * p.max_pages;
+  int32_t* rd = p.table + (int64_t)dst * p.max_pages;
+  for (int j = threadIdx.x; j < npg; j += blockDim.x) {
+    const int page = rs[j];
+    rd[j] = page;
+    p.refcount[page] += 1;  // a sequence's pages are distinct: no two threads share one
+  }
+  if (threadIdx.x == 0) {
+    p.held[dst] = npg;
+    p.base[dst] = npg;
+  }
+}
+
+// Copy [2][Hkv][n][D] keys/values of tokens pos0.. into the sequence's pages.
+__global__ void k_kv_load(PoolDev p, KvGeom g, int seq, int layer, int pos0, int n,
+                          const bf16_t* src) {
+  const int64_t total = (int64_t)2 * g.n_kv_heads * n * g.head_dim;
+  const int32_t* row = p.table + (int64_t)seq * p.max_pages;
+  for (int64_t e = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; e < total;
+       e += (int64_t)gridDim.x * blockDim.x) {
+    const int d = (int)(e % g.head_dim);
+    const int64_t r = e / g.head_dim;
+    const int tkn = (int)(r % n);
+    const int kvh = (int)((r / n) % g.n_kv_heads);
+    const int kind = (int)(r / ((int64_t)n * g.n_kv_heads));
+    const int pos = pos0 + tkn;
+    const int page = row[pos / p.page_size], slot = pos % p.page_size;
+    bf16_t* base = g.kv + g.page_elems(layer, page, kvh, kind);
+    const int64_t o = kind == 0 ? (int64_t)slot * g.head_dim + d : (int64_t)d * p.page_size + slot;
+    base[o] = src[e];
+  }
+}
+
+// ctx_lens[i] += n_new[i] (prefill bookkeeping, device side).
+__global__ void k_add_ctx(int n, int32_t* ctx, const int32_t* add) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) ctx[i] += add[i];
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------- launchers
+void launch_pool_init(const PoolDev& p, hipStream_t st) {
+  k_pool_init<<<1024, 256, 0, st>>>(p);
+}
+void launch_grow(const PoolDev& p, int n, const int32_t* seq, const int32_t* a, const int32_t* b,
+                 int mode, hipStream_t st) {
+  k_grow<<<1, kBT, 0, st>>>(p, n, seq, a, b, mode);
+}
+void launch_verify_setup(const PoolDev& p, const VerifySetupArgs& a, const StepMeta& m,
+                         hipStream_t st) {
+  k_verify_setup<<<1, kBT, 0, st>>>(p, a, m);
+}
+void launch_commit(const PoolDev& p, int B, const int32_t* seq, int32_t* ctx, const int32_t* acc,
+                   hipStream_t st) {
+  k_commit<<<1, kBT, 0, st>>>(p, B, seq, ctx, acc);
+}
+void launch_free(const PoolDev& p, int n, const int32_t* seq, hipStream_t st) {
+  k_free<<<1, kBT, 0, st>>>(p, n, seq);
+}
+void launch_fork(const PoolDev& p, int src, int dst, int npg, hipStream_t st) {
+  k_fork<<<1, 1024, 0, st>>>(p, src, dst, npg);
+}
+void launch_kv_load(const PoolDev& p, const KvGeom& g, int seq, int layer, int pos0, int n,
+                    const bf16_t* src, hipStream_t st) {
+  const int64_t total = (int64_t)2 * g.n_kv_heads * n * g.head_dim;
+  const int blocks = (int)std::min<int64_t>((total + 255) / 256, 65536);
+  k_kv_load<<<blocks, 256, 0, st>>>(p, g, seq, layer, pos0, n, src);
+}
+void launch_add_ctx(int n, int32_t* ctx, const int32_t* add, hipStream_t st) {
+  k_add_ctx<<<cdiv_i(n, 256), 256, 0, st>>>(n, ctx, add);
+}

@@ -1,0 +1,98 @@
+// Shared device helpers and internal launch interfaces for the gfx950 kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef uint16_t bf16_t;  // raw bfloat16 bits in memory
+
+#define WAR_DEV __device__ __forceinline__
+
+// ------------------------------------------------------------------ bf16 bits
+WAR_DEV float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// float -> bfloat16 bits, round to nearest even; NaN stays NaN (quietened).
+WAR_DEV bf16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16_t)(u >> 16);
+}
+
+// round a float to the nearest bfloat16 value, kept as float
+WAR_DEV float round_bf(float f) { return bf2f(f2bf(f)); }
+
+WAR_DEV uint32_t pack2(float a, float b) {
+  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+}
+
+WAR_DEV bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+WAR_DEV f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// ------------------------------------------------------------ wave reductions
+WAR_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+WAR_DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Block-wide sum over blockDim.x (multiple of 64, <= 1024) threads.
+WAR_DEV float block_sum(float v, float* red /* [16] shared */) {
+  v = wave_sum(v);
+  const int w = threadIdx.x >> 6, l = threadIdx.x & 63, nw = blockDim.x >> 6;
+  __syncthreads();
+  if (l == 0) red[w] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int i = 0; i < nw; ++i) t += red[i];
+  return t;
+}
+
+__host__ __device__ inline int cdiv_i(int a, int b) { return (a + b - 1) / b; }
+
+// ---------------------------------------------------------- internal layouts
+// Pool device state (one allocation, see PoolDev below).
+struct PoolDev {
+  int32_t* stack;      // [num_pages] free stack, top at stack[free_count-1]
+  int32_t* refcount;   // [num_pages]
+  int32_t* held;       // [max_seqs] pages held per sequence
+  int32_t* base;       // [max_seqs] pages held before the last reservation
+  int32_t* scalars;    // [0] free_count, [1] error flags
+  int32_t* table;      // [max_seqs][max_pages] (caller memory)
+  int32_t num_pages, max_seqs, max_pages, page_size;
+};
+
+// Per-forward row metadata built on the device (verify) or host (prefill).
+//   rows:     tok[r], pos[r], active[r] for r < n_rows
+//   requests: seq[b], pos0[b] (position of the request's first row),
+//             ntok[b] (active rows), row0[b] (row of token 0)
+//   attention work list: items[i] = (b, row_block, key_chunk, 0), n_items,
+//             segment (b, row_block) -> first item and item count
+struct StepMeta {
+  int32_t* tok;
+  int32_t* pos;
+  int32_t* active;
+  int32_t* row_req;     // request index of each row
+  int32_t* req_seq;
+  int32_t* req_pos0;
+  int32_t* req_ntok;
+  int32_t* req_row0;
+  int4* items;
+  int32_t* n_items;     // [1]
+  int32_t* seg_begin;   // [n_segs]
+  int32_t* seg_count;   // [n_segs]
+  int32_t* seg_req;     // [n_segs]
+  int32_t* seg_rb;      // [n_segs]
+};
+
+enum { ERR_BAD_TOKEN = 1, ERR_NO_PAGES = 2 };

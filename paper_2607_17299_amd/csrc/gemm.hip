@@ -1,0 +1,226 @@
+// Skinny-M bf16 GEMM on gfx950 MFMA for the decoder projections and the LM head.
+//
+// C[m][n] = sum_k A[m][k] * W[n][k]: A is the (few-row) activation matrix,
+// W a weight matrix stored [out][in].  In the verify step M is 4..~600 rows
+// against N x K weights of 16-310 MB, so the kernel is bound by streaming W
+// from HBM: every weight byte is read exactly once per m-block.
+//
+// Workgroup = 4 waves = 128 output columns; each wave owns 32 columns (two
+// 16-wide MFMA n-tiles) and all MT 16-row m-tiles of the workgroup's m-block.
+// K advances in steps of 64:
+//   * W goes straight from HBM to registers -- each lane reads 32 contiguous
+//     bytes of two W rows per step (4 lanes cover a 128-byte line) -- with three
+//     steps in flight;
+//   * the A tile (MT*16 rows x 64) is staged through LDS (double-buffered,
+//     rows padded to 144 bytes) and shared by the 4 waves;
+//   * v_mfma_f32_16x16x32_bf16 accumulates in fp32.  Inside a step the
+//     k-index is permuted identically for A and W (lane group g holds k
+//     g*16 .. g*16+15), which leaves the dot products unchanged.
+// Split-K over blockIdx.y fills the 256 CUs when N is small; partial sums go to
+// P[split][M][N] and a row kernel adds them in a fixed order (deterministic).
+// The argmax epilogue (LM head, one split) writes optional fp32 logits and the
+// best (value, lowest index) of each row within each 128-column block.
+#include "kernels.h"
+
+namespace {
+
+constexpr int KS = 64;
+constexpr int ROWB = KS * 2 + 16;  // LDS bytes per A row (16-byte pad vs bank conflicts)
+
+template <int MT>
+struct Tile {
+  static constexpr int CHUNKS = MT * 16 * (KS / 8);  // 16-byte chunks of the A tile
+  static constexpr int PER_THREAD = (CHUNKS + 255) / 256;
+  static constexpr int BYTES = MT * 16 * ROWB;
+};
+
+template <int MT, int EPI>
+__global__ void __launch_bounds__(256) k_gemm(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) unsigned char sA[2][Tile<MT>::BYTES];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
+  const int split = blockIdx.y;
+  const int m0 = blockIdx.z * MT * 16;
+  const int kb = split * g.kper;
+  const int ke = min(g.K, kb + g.kper);
+  const int nsteps = (ke - kb) / KS;
+  const int n0 = blockIdx.x * 128;
+  const bf16_t* Wb = n0 < g.n_split ? g.W1 + (int64_t)n0 * g.ldw
+                                    : g.W2 + (int64_t)(n0 - g.n_split) * g.ldw;
+  const bf16_t* w0 = Wb + (int64_t)(w * 32 + ln) * g.ldw + kb + lg * 16;
+  const bf16_t* w1 = w0 + (int64_t)16 * g.ldw;
+
+  // A rows this thread stages (fixed across steps)
+  const bf16_t* arow[Tile<MT>::PER_THREAD];
+  int aoff[Tile<MT>::PER_THREAD];
+#pragma unroll
+  for (int i = 0; i < Tile<MT>::PER_THREAD; ++i) {
+    const int c = tid + 256 * i;
+    const int r = c >> 3, q = c & 7;
+    const int gm = m0 + r;
+    arow[i] = nullptr;
+    aoff[i] = r * ROWB + q * 16;
+    if (c < Tile<MT>::CHUNKS && gm < g.M) {
+      const int src = g.a_rows ? g.a_rows[gm] : gm;
+      arow[i] = g.A + (int64_t)src * g.lda + kb + q * 8;
+    }
+  }
+
+  auto load_w = [&](uint4* wr, int s) {
+    const int k = s * KS;
+    wr[0] = *reinterpret_cast<const uint4*>(w0 + k);
+    wr[1] = *reinterpret_cast<const uint4*>(w0 + k + 8);
+    wr[2] = *reinterpret_cast<const uint4*>(w1 + k);
+    wr[3] = *reinterpret_cast<const uint4*>(w1 + k + 8);
+  };
+  uint4 ar[Tile<MT>::PER_THREAD];
+  auto load_a = [&](int s) {
+#pragma unroll
+    for (int i = 0; i < Tile<MT>::PER_THREAD; ++i)
+      ar[i] = arow[i] ? *reinterpret_cast<const uint4*>(arow[i] + s * KS) : make_uint4(0, 0, 0, 0);
+  };
+  auto store_a = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < Tile<MT>::PER_THREAD; ++i)
+      if (tid + 256 * i < Tile<MT>::CHUNKS)
+        *reinterpret_cast<uint4*>(&sA[buf][aoff[i]]) = ar[i];
+  };
+
+  f32x4 acc[MT][2];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) acc[mt][0] = acc[mt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](const uint4* wr, int buf) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const bf16x8 b0 = as_bf16x8(wr[j]), b1 = as_bf16x8(wr[2 + j]);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const bf16x8 a = as_bf16x8(
+            *reinterpret_cast<const uint4*>(&sA[buf][(mt * 16 + ln) * ROWB + lg * 32 + j * 16]));
+        acc[mt][0] = mfma16(a, b0, acc[mt][0]);
+        acc[mt][1] = mfma16(a, b1, acc[mt][1]);
+      }
+    }
+  };
+
+  uint4 wA[4], wB[4], wC[4];
+  if (nsteps > 0) load_w(wA, 0);
+  if (nsteps > 1) load_w(wB, 1);
+  if (nsteps > 2) load_w(wC, 2);
+  if (nsteps > 0) {
+    load_a(0);
+    store_a(0);
+  }
+  __syncthreads();
+
+#define GEMM_STEP(WR, S)                         \
+  if ((S) < nsteps) {                            \
+    if ((S) + 1 < nsteps) load_a((S) + 1);       \
+    compute(WR, (S)&1);                          \
+    if ((S) + 3 < nsteps) load_w(WR, (S) + 3);   \
+    if ((S) + 1 < nsteps) store_a(((S) + 1) & 1); \
+    __syncthreads();                             \
+  }
+  for (int s = 0; s < nsteps; s += 3) {
+    GEMM_STEP(wA, s)
+    GEMM_STEP(wB, s + 1)
+    GEMM_STEP(wC, s + 2)
+  }
+#undef GEMM_STEP
+
+  // lane holds C[mt*16 + lg*4 + i][n0 + w*32 + t*16 + ln]
+  if constexpr (EPI == EPI_PARTIAL) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = m0 + mt * 16 + lg * 4 + i;
+          if (m < g.M)
+            g.P[((int64_t)split * g.M + m) * g.N + n0 + w * 32 + t * 16 + ln] = acc[mt][t][i];
+        }
+  } else {
+    float* sv = reinterpret_cast<float*>(&sA[0][0]);           // [4][MT*16]
+    int* si = reinterpret_cast<int*>(&sA[1][0]);                // [4][MT*16]
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = mt * 16 + lg * 4 + i;
+        const int m = m0 + r;
+        const int c0 = n0 + w * 32 + ln, c1 = c0 + 16;
+        float v = acc[mt][0][i];
+        int idx = c0;
+        const float v1 = acc[mt][1][i];
+        if (v1 > v) {
+          v = v1;
+          idx = c1;
+        }
+        if (g.logits && m < g.M) {
+          g.logits[(int64_t)m * g.ld_logits + c0] = acc[mt][0][i];
+          g.logits[(int64_t)m * g.ld_logits + c1] = acc[mt][1][i];
+        }
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) {
+          const float ov = __shfl_xor(v, o, 64);
+          const int oi = __shfl_xor(idx, o, 64);
+          if (ov > v || (ov == v && oi < idx)) {
+            v = ov;
+            idx = oi;
+          }
+        }
+        if (ln == 0) {
+          sv[w * MT * 16 + r] = v;
+          si[w * MT * 16 + r] = idx;
+        }
+      }
+    __syncthreads();
+    for (int r = tid; r < MT * 16; r += 256) {
+      const int m = m0 + r;
+      if (m >= g.M) continue;
+      float v = sv[r];
+      int idx = si[r];
+      for (int ww = 1; ww < 4; ++ww) {
+        const float ov = sv[ww * MT * 16 + r];
+        const int oi = si[ww * MT * 16 + r];
+        if (ov > v || (ov == v && oi < idx)) {
+          v = ov;
+          idx = oi;
+        }
+      }
+      g.amax_v[(int64_t)m * gridDim.x + blockIdx.x] = v;
+      g.amax_i[(int64_t)m * gridDim.x + blockIdx.x] = idx;
+    }
+  }
+}
+
+template <int MT>
+void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
+  dim3 grid(g.N / 128, splits, cdiv_i(g.M, MT * 16));
+  if (epi == EPI_PARTIAL)
+    k_gemm<MT, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+  else
+    k_gemm<MT, EPI_ARGMAX><<<grid, 256, 0, st>>>(g);
+}
+
+}  // namespace
+
+int gemm_mt(int M) { return std::min(12, std::max(1, cdiv_i(M, 16))); }
+
+void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st) {
+  switch (gemm_mt(g.M)) {
+    case 1: launch_mt<1>(g, epi, splits, st); break;
+    case 2: launch_mt<2>(g, epi, splits, st); break;
+    case 3: launch_mt<3>(g, epi, splits, st); break;
+    case 4: launch_mt<4>(g, epi, splits, st); break;
+    case 5: launch_mt<5>(g, epi, splits, st); break;
+    case 6: launch_mt<6>(g, epi, splits, st); break;
+    case 7: launch_mt<7>(g, epi, splits, st); break;
+    case 8: launch_mt<8>(g, epi, splits, st); break;
+    case 9: launch_mt<9>(g, epi, splits, st); break;
+    case 10: launch_mt<10>(g, epi, splits, st); break;
+    case 11: launch_mt<11>(g, epi, splits, st); break;
+    default: launch_mt<12>(g, epi, splits, st); break;
+  }
+}

@@ -1,0 +1,108 @@
+// Internal launch interface between the C-ABI runtime and the gfx950 kernels.
+#pragma once
+
+#include <algorithm>
+
+#include "common.h"
+
+// Geometry of the paged KV storage:
+//   element offset of page `page`, layer `layer`, kv-head `kvh`, kind (0 = K, 1 = V^T)
+//   = ((((layer * num_pages + page) * n_kv_heads + kvh) * 2 + kind) * page_size * head_dim
+// K is stored [page_size][head_dim]; V transposed, [head_dim][page_size].
+struct KvGeom {
+  bf16_t* kv;
+  int64_t num_pages;
+  int n_kv_heads, head_dim, page_size;
+  __host__ __device__ int64_t page_elems(int layer, int page, int kvh, int kind) const {
+    return ((((int64_t)layer * num_pages + page) * n_kv_heads + kvh) * 2 + kind) *
+           (int64_t)page_size * head_dim;
+  }
+};
+
+struct VerifySetupArgs {
+  int B, k_max, vocab, chunk;
+  const int32_t* seq_ids;
+  const int32_t* ctx_lens;
+  const int32_t* last_tokens;
+  const int32_t* draft_tokens;
+  const int32_t* draft_lens;
+};
+
+// C[m][n] = sum_k A[arow(m)][k] * W[n][k]   (bf16 in, fp32 accumulate)
+// W rows n < n_split come from W1, rows >= n_split from W2 (row n - n_split).
+struct GemmArgs {
+  const bf16_t* A;
+  int lda;
+  const int32_t* a_rows;  // nullable: A row m -> a_rows[m]
+  const bf16_t* W1;
+  const bf16_t* W2;
+  int n_split, ldw;
+  int M, N, K, kper;
+  float* P;  // partial sums [split][M][N]
+  // argmax epilogue (split == 1): per (row, 128-column block) best value and index
+  float* logits;  // nullable [M][ld_logits]
+  int64_t ld_logits;
+  float* amax_v;
+  int32_t* amax_i;
+};
+
+enum { EPI_PARTIAL = 0, EPI_ARGMAX = 1 };
+
+struct AttnArgs {
+  const bf16_t* q;  // [rows][n_q_heads * head_dim]
+  int q_stride;
+  KvGeom kv;
+  int layer;
+  const int32_t* table;
+  int max_pages;
+  StepMeta meta;
+  int G, TB, chunk, n_kv_heads;
+  float scale_log2;  // log2(e) / sqrt(head_dim)
+  float* pm;         // [item][kvh][RB]
+  float* pl;         // [item][kvh][RB]
+  float* po;         // [item][kvh][RB][head_dim]
+  bf16_t* o;         // combine output [rows][n_q_heads * head_dim]
+};
+
+// allocator / setup (alloc.hip)
+void launch_pool_init(const PoolDev& p, hipStream_t st);
+void launch_grow(const PoolDev& p, int n, const int32_t* seq, const int32_t* a, const int32_t* b,
+                 int mode, hipStream_t st);
+void launch_verify_setup(const PoolDev& p, const VerifySetupArgs& a, const StepMeta& m,
+                         hipStream_t st);
+void launch_commit(const PoolDev& p, int B, const int32_t* seq, int32_t* ctx, const int32_t* acc,
+                   hipStream_t st);
+void launch_free(const PoolDev& p, int n, const int32_t* seq, hipStream_t st);
+void launch_fork(const PoolDev& p, int src, int dst, int npg, hipStream_t st);
+void launch_kv_load(const PoolDev& p, const KvGeom& g, int seq, int layer, int pos0, int n,
+                    const bf16_t* src, hipStream_t st);
+void launch_add_ctx(int n, int32_t* ctx, const int32_t* add, hipStream_t st);
+
+// GEMM (gemm.hip)
+int gemm_mt(int M);  // 16-row tiles per workgroup for M rows
+void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st);
+
+// attention (attn.hip)
+int attn_rows_per_block(int G, int k_rows);  // RB (16, 32 or 48)
+void launch_attn(const AttnArgs& a, int RB, int head_dim, int grid, hipStream_t st);
+void launch_attn_combine(const AttnArgs& a, int RB, int head_dim, int n_segs, hipStream_t st);
+
+// elementwise / row kernels (rows.hip)
+struct ModelDims {
+  int d, nq, nkv, hd, F, V, qkv;
+  float eps;
+};
+void launch_rope_table(int rows, const int32_t* pos, const double* inv_freq, int half, float* cos_t,
+                       float* sin_t, hipStream_t st);
+void launch_embed_norm(int rows, const int32_t* tok, const bf16_t* E, const bf16_t* g, int d,
+                       float eps, float* h, bf16_t* u, hipStream_t st);
+void launch_residual_norm(int rows, int splits, const float* P, int d, const bf16_t* g, float eps,
+                          float* h, bf16_t* u, hipStream_t st);
+void launch_qkv_rope(int rows, int splits, const float* P, const ModelDims& md,
+                     const float* cos_t, const float* sin_t, const StepMeta& meta,
+                     const int32_t* row_req, const int32_t* table, int max_pages, const KvGeom& kv,
+                     int layer, bf16_t* q, hipStream_t st);
+void launch_swiglu(int rows, int splits, const float* P, int F, bf16_t* y, hipStream_t st);
+void launch_argmax_accept(int n_req, const int32_t* ntok, int row_stride, int n_blocks,
+                          const float* amax_v, const int32_t* amax_i, const int32_t* draft_tokens,
+                          int k_max, int32_t* accept_lens, int32_t* next_tokens, hipStream_t st);

@@ -1,0 +1,263 @@
+// Row-wise kernels of the decoder step: RoPE table, embedding + RMSNorm,
+// split-K reduction fused with residual + RMSNorm, with RoPE + KV-page write,
+// and with SwiGLU; and the argmax + greedy acceptance of the verify step.
+//
+// Rounding points (bf16 compute, fp32 accumulate): every value that feeds a
+// matrix multiply (norm outputs, SwiGLU product) and the rotated q, k and the v
+// stored in the KV pages are rounded to bf16 (nearest even).  The residual
+// stream, norm statistics, rotation and SwiGLU arithmetic stay fp32.
+#include "kernels.h"
+
+namespace {
+
+// cos/sin of pos * inv_freq[j], evaluated in double and stored as float.
+__global__ void k_rope_table(int rows, const int32_t* pos, const double* inv_freq, int half,
+                             float* cos_t, float* sin_t) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= rows * half) return;
+  const int r = i / half, j = i % half;
+  const double ang = (double)pos[r] * inv_freq[j];
+  cos_t[i] = (float)cos(ang);
+  sin_t[i] = (float)sin(ang);
+}
+
+// u = bf16(h * rsqrt(mean(h^2) + eps) * g), h already in global memory.
+__device__ void norm_row(const float* h, int d, const bf16_t* g, float eps, bf16_t* u, float ss,
+                         float* red) {
+  const float tot = block_sum(ss, red);
+  const float rs = rsqrtf(tot / (float)d + eps);
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    const float4 x = *reinterpret_cast<const float4*>(h + c);
+    const uint2 gg = *reinterpret_cast<const uint2*>(g + c);
+    const float g0 = bf2f(gg.x & 0xffff), g1 = bf2f(gg.x >> 16);
+    const float g2 = bf2f(gg.y & 0xffff), g3 = bf2f(gg.y >> 16);
+    uint2 o;
+    o.x = pack2(x.x * rs * g0, x.y * rs * g1);
+    o.y = pack2(x.z * rs * g2, x.w * rs * g3);
+    *reinterpret_cast<uint2*>(u + c) = o;
+  }
+}
+
+__global__ void __launch_bounds__(256) k_embed_norm(const int32_t* tok, const bf16_t* E,
+                                                    const bf16_t* g, int d, float eps, float* h,
+                                                    bf16_t* u) {
+  __shared__ float red[16];
+  const int r = blockIdx.x;
+  const bf16_t* e = E + (int64_t)tok[r] * d;
+  float* hr = h + (int64_t)r * d;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    const uint2 v = *reinterpret_cast<const uint2*>(e + c);
+    float4 x;
+    x.x = bf2f(v.x & 0xffff);
+    x.y = bf2f(v.x >> 16);
+    x.z = bf2f(v.y & 0xffff);
+    x.w = bf2f(v.y >> 16);
+    ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+    *reinterpret_cast<float4*>(hr + c) = x;
+  }
+  norm_row(hr, d, g, eps, u + (int64_t)r * d, ss, red);
+}
+
+// h += sum_s P[s]; u = norm(h) * g
+__global__ void __launch_bounds__(256) k_residual_norm(int rows, int splits, const float* P, int d,
+                                                       const bf16_t* g, float eps, float* h,
+                                                       bf16_t* u) {
+  __shared__ float red[16];
+  const int r = blockIdx.x;
+  float* hr = h + (int64_t)r * d;
+  float ss = 0.f;
+  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+    float4 x = *reinterpret_cast<const float4*>(hr + c);
+    for (int s = 0; s < splits; ++s) {
+      const float4 p = *reinterpret_cast<const float4*>(P + ((int64_t)s * rows + r) * d + c);
+      x.x += p.x;
+      x.y += p.y;
+      x.z += p.z;
+      x.w += p.w;
+    }
+    ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+    *reinterpret_cast<float4*>(hr + c) = x;
+  }
+  norm_row(hr, d, g, eps, u + (int64_t)r * d, ss, red);
+}
+
+// Sum the QKV partials of one row, rotate q and k (rotate-half pairs (j, j+D/2)),
+// round to bf16; q goes to its buffer, k and v of active rows into the KV page slot
+// of the row's position.
+__global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const float* P, ModelDims md,
+                                                  const float* cos_t, const float* sin_t,
+                                                  StepMeta meta, const int32_t* row_req,
+                                                  const int32_t* table, int max_pages, KvGeom kv,
+                                                  int layer, bf16_t* q) {
+  const int r = blockIdx.x;
+  const int half = md.hd / 2;
+  const int nq_pairs = md.nq * half, nk_pairs = md.nkv * half;
+  const int n_pairs = md.qkv / 2;
+  const bool act = meta.active[r] != 0;
+  int page = 0, slot = 0;
+  if (act) {
+    const int pos = meta.pos[r];
+    const int seq = meta.req_seq[row_req[r]];
+    page = table[(int64_t)seq * max_pages + pos / kv.page_size];
+    slot = pos % kv.page_size;
+  }
+  const float* pr = P + (int64_t)r * md.qkv;
+  const int64_t pstride = (int64_t)rows * md.qkv;
+  for (int p = threadIdx.x; p < n_pairs; p += blockDim.x) {
+    int region, head, j;
+    if (p < nq_pairs) {
+      region = 0;
+      head = p / half;
+      j = p % half;
+    } else if (p < nq_pairs + nk_pairs) {
+      region = 1;
+      head = (p - nq_pairs) / half;
+      j = (p - nq_pairs) % half;
+    } else {
+      region = 2;
+      head = (p - nq_pairs - nk_pairs) / half;
+      j = (p - nq_pairs - nk_pairs) % half;
+    }
+    const int col = (region == 0 ? 0 : region == 1 ? md.nq * md.hd : (md.nq + md.nkv) * md.hd) +
+                    head * md.hd + j;
+    float x1 = 0.f, x2 = 0.f;
+    for (int s = 0; s < splits; ++s) {
+      x1 += pr[s * pstride + col];
+      x2 += pr[s * pstride + col + half];
+    }
+    float y1 = x1, y2 = x2;
+    if (region < 2) {
+      const float c = cos_t[r * half + j], sn = sin_t[r * half + j];
+      y1 = x1 * c - x2 * sn;
+      y2 = x2 * c + x1 * sn;
+    }
+    const bf16_t b1 = f2bf(y1), b2 = f2bf(y2);
+    if (region == 0) {
+      bf16_t* qr = q + (int64_t)r * md.nq * md.hd + head * md.hd;
+      qr[j] = b1;
+      qr[j + half] = b2;
+    } else if (act) {
+      bf16_t* base = kv.kv + kv.page_elems(layer, page, head, region - 1);
+      if (region == 1) {
+        base[slot * md.hd + j] = b1;
+        base[slot * md.hd + j + half] = b2;
+      } else {
+        base[j * kv.page_size + slot] = b1;
+        base[(j + half) * kv.page_size + slot] = b2;
+      }
+    }
+  }
+}
+
+// y = bf16(silu(gate) * up); gate = columns [0, F), up = [F, 2F) of the partials
+__global__ void __launch_bounds__(256) k_swiglu(int rows, int splits, const float* P, int F,
+                                                bf16_t* y) {
+  const int r = blockIdx.x;
+  const int64_t N = 2 * (int64_t)F;
+  for (int c = threadIdx.x * 4; c < F; c += blockDim.x * 4) {
+    float4 gt = {0.f, 0.f, 0.f, 0.f}, up = {0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < splits; ++s) {
+      const float* ps = P + ((int64_t)s * rows + r) * N;
+      const float4 a = *reinterpret_cast<const float4*>(ps + c);
+      const float4 b = *reinterpret_cast<const float4*>(ps + F + c);
+      gt.x += a.x; gt.y += a.y; gt.z += a.z; gt.w += a.w;
+      up.x += b.x; up.y += b.y; up.z += b.z; up.w += b.w;
+    }
+    auto sw = [](float a, float b) { return a / (1.f + expf(-a)) * b; };
+    uint2 o;
+    o.x = pack2(sw(gt.x, up.x), sw(gt.y, up.y));
+    o.y = pack2(sw(gt.z, up.z), sw(gt.w, up.w));
+    *reinterpret_cast<uint2*>(y + (int64_t)r * F + c) = o;
+  }
+}
+
+// Per request: greedy token of each active row (best over the LM head's column
+// blocks, ties -> lowest id), then the longest draft prefix that matches.
+__global__ void __launch_bounds__(256) k_argmax_accept(const int32_t* ntok, int row_stride,
+                                                       int n_blocks, const float* amax_v,
+                                                       const int32_t* amax_i,
+                                                       const int32_t* drafts, int k_max,
+                                                       int32_t* accept_lens, int32_t* next_tokens) {
+  __shared__ float sv[4];
+  __shared__ int si[4];
+  __shared__ int greedy[64];
+  const int b = blockIdx.x;
+  const int n = ntok ? min(ntok[b], 64) : 1;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  for (int i = 0; i < n; ++i) {
+    const int64_t row = (int64_t)b * row_stride + i;
+    float v = -INFINITY;
+    int idx = 0x7fffffff;
+    for (int c = threadIdx.x; c < n_blocks; c += blockDim.x) {
+      const float ov = amax_v[row * n_blocks + c];
+      const int oi = amax_i[row * n_blocks + c];
+      if (ov > v || (ov == v && oi < idx)) {
+        v = ov;
+        idx = oi;
+      }
+    }
+#pragma unroll
+    for (int o = 32; o >= 1; o >>= 1) {
+      const float ov = __shfl_xor(v, o, 64);
+      const int oi = __shfl_xor(idx, o, 64);
+      if (ov > v || (ov == v && oi < idx)) {
+        v = ov;
+        idx = oi;
+      }
+    }
+    if (lane == 0) {
+      sv[w] = v;
+      si[w] = idx;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+      for (int ww = 1; ww < 4; ++ww)
+        if (sv[ww] > v || (sv[ww] == v && si[ww] < idx)) {
+          v = sv[ww];
+          idx = si[ww];
+        }
+      greedy[i] = idx;
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    int a = 0;
+    if (n > 0) {
+      while (a < n - 1 && drafts && drafts[(int64_t)b * k_max + a] == greedy[a]) ++a;
+    }
+    if (accept_lens) accept_lens[b] = a;
+    next_tokens[b] = n > 0 ? greedy[a] : -1;
+  }
+}
+
+}  // namespace
+
+void launch_rope_table(int rows, const int32_t* pos, const double* inv_freq, int half, float* cos_t,
+                       float* sin_t, hipStream_t st) {
+  k_rope_table<<<cdiv_i(rows * half, 256), 256, 0, st>>>(rows, pos, inv_freq, half, cos_t, sin_t);
+}
+void launch_embed_norm(int rows, const int32_t* tok, const bf16_t* E, const bf16_t* g, int d,
+                       float eps, float* h, bf16_t* u, hipStream_t st) {
+  k_embed_norm<<<rows, 256, 0, st>>>(tok, E, g, d, eps, h, u);
+}
+void launch_residual_norm(int rows, int splits, const float* P, int d, const bf16_t* g, float eps,
+                          float* h, bf16_t* u, hipStream_t st) {
+  k_residual_norm<<<rows, 256, 0, st>>>(rows, splits, P, d, g, eps, h, u);
+}
+void launch_qkv_rope(int rows, int splits, const float* P, const ModelDims& md,
+                     const float* cos_t, const float* sin_t, const StepMeta& meta,
+                     const int32_t* row_req, const int32_t* table, int max_pages, const KvGeom& kv,
+                     int layer, bf16_t* q, hipStream_t st) {
+  k_qkv_rope<<<rows, 256, 0, st>>>(rows, splits, P, md, cos_t, sin_t, meta, row_req, table,
+                                   max_pages, kv, layer, q);
+}
+void launch_swiglu(int rows, int splits, const float* P, int F, bf16_t* y, hipStream_t st) {
+  k_swiglu<<<rows, 256, 0, st>>>(rows, splits, P, F, y);
+}
+void launch_argmax_accept(int n_req, const int32_t* ntok, int row_stride, int n_blocks,
+                          const float* amax_v, const int32_t* amax_i, const int32_t* draft_tokens,
+                          int k_max, int32_t* accept_lens, int32_t* next_tokens, hipStream_t st) {
+  k_argmax_accept<<<n_req, 256, 0, st>>>(ntok, row_stride, n_blocks, amax_v, amax_i, draft_tokens,
+                                         k_max, accept_lens, next_tokens);
+}

@@ -1,0 +1,813 @@
+// C-ABI runtime: model and KV-pool objects, argument checks, page-capacity
+// tracking, and the orchestration of the verify step, commit and prefill-append
+// as sequences of gfx950 kernels on the caller's stream.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <unordered_set>
+#include <vector>
+
+#include "../../include/war.h"
+#include "kernels.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+war_status fail(war_status code, const std::string& msg) {
+  g_err = msg;
+  return code;
+}
+
+#define HIPCHK(x)                                                            \
+  do {                                                                       \
+    hipError_t e_ = (x);                                                     \
+    if (e_ != hipSuccess)                                                    \
+      return fail(WAR_ERR_HIP, std::string(#x) + ": " + hipGetErrorString(e_)); \
+  } while (0)
+
+#define CHECK(cond, msg)                          \
+  do {                                            \
+    if (!(cond)) return fail(WAR_ERR_INVALID_ARG, msg); \
+  } while (0)
+
+// Grow-only device buffer.
+struct DevBuf {
+  void* p = nullptr;
+  size_t bytes = 0;
+  hipError_t ensure(size_t n) {
+    if (n <= bytes) return hipSuccess;
+    if (p) {
+      hipError_t e = hipFree(p);
+      if (e != hipSuccess) return e;
+      p = nullptr;
+      bytes = 0;
+    }
+    hipError_t e = hipMalloc(&p, n);
+    if (e == hipSuccess) bytes = n;
+    return e;
+  }
+  void release() {
+    if (p) (void)hipFree(p);
+    p = nullptr;
+    bytes = 0;
+  }
+  template <class T>
+  T* as() const {
+    return static_cast<T*>(p);
+  }
+};
+
+struct LayerW {
+  const bf16_t *attn_norm, *w_qkv, *w_o, *ffn_norm, *w_gate, *w_up, *w_down;
+};
+
+constexpr int kMaxBatch = 1024;
+constexpr int kPrefillChunk = 1024;  // keys per attention item when prefilling
+constexpr int64_t kPartialCap = int64_t(64) << 20;  // fp32 split-K partial elements
+
+}  // namespace
+
+struct war_model {
+  war_model_config cfg;
+  ModelDims md;
+  const bf16_t* embed;
+  std::vector<LayerW> layers;
+  const bf16_t* final_norm;
+  const bf16_t* w_lm;
+  int max_rows;
+  // workspace
+  DevBuf h, u, q, o, P, cos_t, sin_t, inv_freq, amax_v, amax_i;
+  DevBuf rows_i32;  // tok, pos, active, row_req  [4][max_rows]
+  DevBuf reqs_i32;  // seq, pos0, ntok, row0      [4][n_req_cap]
+  DevBuf segs_i32;  // begin, count, req, rb      [4][n_seg_cap]
+  DevBuf n_items, items, pm, pl, po, a_rows;
+  int n_req_cap, n_seg_cap;
+  std::vector<int32_t> h_stage;  // host staging for prefill metadata
+  DevBuf stage_dev;              // device copy of per-prefill host arrays
+  int32_t* pinned = nullptr;     // pinned host staging
+  size_t pinned_ints = 0;
+
+  StepMeta meta() const {
+    StepMeta m;
+    int32_t* r = rows_i32.as<int32_t>();
+    m.tok = r;
+    m.pos = r + max_rows;
+    m.active = r + 2 * max_rows;
+    m.row_req = r + 3 * max_rows;
+    int32_t* q4 = reqs_i32.as<int32_t>();
+    m.req_seq = q4;
+    m.req_pos0 = q4 + n_req_cap;
+    m.req_ntok = q4 + 2 * n_req_cap;
+    m.req_row0 = q4 + 3 * n_req_cap;
+    m.items = items.as<int4>();
+    m.n_items = n_items.as<int32_t>();
+    int32_t* s4 = segs_i32.as<int32_t>();
+    m.seg_begin = s4;
+    m.seg_count = s4 + n_seg_cap;
+    m.seg_req = s4 + 2 * n_seg_cap;
+    m.seg_rb = s4 + 3 * n_seg_cap;
+    return m;
+  }
+};
+
+struct war_kv_pool {
+  war_model_config cfg;
+  KvGeom geom;
+  PoolDev dev;
+  DevBuf state;    // stack | refcount | held | base | scalars
+  DevBuf tmp;      // device copies of host id arrays
+  int32_t* pinned = nullptr;
+  size_t pinned_ints = 0;
+  int64_t free_lb;  // host lower bound of the device free count
+  bool pending = false;
+  int pending_B = 0;
+};
+
+namespace {
+
+hipError_t ensure_pinned(int32_t*& p, size_t& cap, size_t n) {
+  if (n <= cap) return hipSuccess;
+  if (p) (void)hipHostFree(p);
+  p = nullptr;
+  cap = 0;
+  hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&p), n * sizeof(int32_t), hipHostMallocDefault);
+  if (e == hipSuccess) cap = n;
+  return e;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+war_status check_config(const war_model_config* c) {
+  if (!c) return fail(WAR_ERR_INVALID_ARG, "null config");
+  if (c->n_layers < 1 || c->d_model < 1 || c->n_q_heads < 1 || c->n_kv_heads < 1 ||
+      c->head_dim < 1 || c->ffn_dim < 1 || c->vocab < 1 || c->max_rows < 1)
+    return fail(WAR_ERR_INVALID_ARG, "non-positive dimension in config");
+  if (c->n_q_heads % c->n_kv_heads) return fail(WAR_ERR_INVALID_ARG, "n_q_heads % n_kv_heads != 0");
+  const int G = c->n_q_heads / c->n_kv_heads;
+  const int qkv = (c->n_q_heads + 2 * c->n_kv_heads) * c->head_dim;
+  if (c->d_model % 128 || c->ffn_dim % 128 || c->vocab % 128 || qkv % 128 ||
+      (c->n_q_heads * c->head_dim) % 128)
+    return fail(WAR_ERR_UNSUPPORTED, "d_model, ffn_dim, vocab and projection widths must be multiples of 128");
+  if (c->head_dim != 64 && c->head_dim != 128) return fail(WAR_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
+  if (G > 8) return fail(WAR_ERR_UNSUPPORTED, "more than 8 query heads per kv head");
+  if (c->page_size != 16) return fail(WAR_ERR_UNSUPPORTED, "page_size must be 16");
+  if (c->max_rows > 65536) return fail(WAR_ERR_UNSUPPORTED, "max_rows > 65536");
+  if (!(c->rms_eps >= 0.f) || !(c->rope_base > 0.f)) return fail(WAR_ERR_INVALID_ARG, "bad eps or rope base");
+  return WAR_OK;
+}
+
+bool same_shape(const war_model_config& a, const war_model_config& b) {
+  return a.n_layers == b.n_layers && a.n_kv_heads == b.n_kv_heads && a.head_dim == b.head_dim &&
+         a.page_size == b.page_size;
+}
+
+struct Split {
+  int s, kper;
+};
+
+Split pick_split(int M, int N, int K, int64_t cap_elems) {
+  const int mt = gemm_mt(M);
+  const int mblocks = cdiv_i(M, mt * 16);
+  const int base = (N / 128) * mblocks;
+  int s = std::max(1, (int)std::lround(1024.0 / base));
+  s = std::min(s, std::max(1, K / 256));
+  while (s > 1 && (int64_t)s * M * N > cap_elems) --s;
+  int kper = cdiv_i(cdiv_i(K, s), 64) * 64;
+  s = cdiv_i(K, kper);
+  return {s, kper};
+}
+
+// One projection: P[split][M][N] = A x W^T (or the LM-head argmax epilogue).
+war_status gemm(war_model* m, const bf16_t* A, int lda, const int32_t* a_rows, const bf16_t* W1,
+                const bf16_t* W2, int n_split, int M, int N, int K, int* splits_out,
+                hipStream_t st, bool argmax = false, float* logits = nullptr) {
+  GemmArgs g{};
+  g.A = A;
+  g.lda = lda;
+  g.a_rows = a_rows;
+  g.W1 = W1;
+  g.W2 = W2 ? W2 : W1;
+  g.n_split = W2 ? n_split : N;
+  g.ldw = K;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  Split sp{1, K};
+  if (!argmax) sp = pick_split(M, N, K, (int64_t)(m->P.bytes / 4));
+  g.kper = sp.kper;
+  g.P = m->P.as<float>();
+  g.logits = logits;
+  g.ld_logits = N;
+  g.amax_v = m->amax_v.as<float>();
+  g.amax_i = m->amax_i.as<int32_t>();
+  launch_gemm(g, argmax ? EPI_ARGMAX : EPI_PARTIAL, sp.s, st);
+  if (splits_out) *splits_out = sp.s;
+  return WAR_OK;
+}
+
+// The decoder body over `R` rows whose metadata is in m->meta(); the final
+// normalised hidden state ends in m->u.
+war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_base, int RB,
+                      int attn_grid, int n_segs, hipStream_t st) {
+  const ModelDims& md = m->md;
+  const StepMeta meta = m->meta();
+  float* h = m->h.as<float>();
+  bf16_t* u = m->u.as<bf16_t>();
+  bf16_t* q = m->q.as<bf16_t>();
+  bf16_t* o = m->o.as<bf16_t>();
+  float* P = m->P.as<float>();
+  launch_rope_table(R, meta.pos, m->inv_freq.as<double>(), md.hd / 2, m->cos_t.as<float>(),
+                    m->sin_t.as<float>(), st);
+  launch_embed_norm(R, meta.tok, m->embed, m->layers[0].attn_norm, md.d, md.eps, h, u, st);
+  for (int l = 0; l < m->cfg.n_layers; ++l) {
+    const LayerW& L = m->layers[l];
+    int s = 1;
+    gemm(m, u, md.d, nullptr, L.w_qkv, nullptr, 0, R, md.qkv, md.d, &s, st);
+    launch_qkv_rope(R, s, P, md, m->cos_t.as<float>(), m->sin_t.as<float>(), meta, meta.row_req,
+                    p->dev.table, p->dev.max_pages, p->geom, l, q, st);
+    AttnArgs a = attn_base;
+    a.layer = l;
+    launch_attn(a, RB, md.hd, attn_grid, st);
+    launch_attn_combine(a, RB, md.hd, n_segs, st);
+    gemm(m, o, md.nq * md.hd, nullptr, L.w_o, nullptr, 0, R, md.d, md.nq * md.hd, &s, st);
+    launch_residual_norm(R, s, P, md.d, L.ffn_norm, md.eps, h, u, st);
+    gemm(m, u, md.d, nullptr, L.w_gate, L.w_up, md.F, R, 2 * md.F, md.d, &s, st);
+    launch_swiglu(R, s, P, md.F, u, st);
+    gemm(m, u, md.F, nullptr, L.w_down, nullptr, 0, R, md.d, md.F, &s, st);
+    const bf16_t* gnext = l + 1 < m->cfg.n_layers ? m->layers[l + 1].attn_norm : m->final_norm;
+    launch_residual_norm(R, s, P, md.d, gnext, md.eps, h, u, st);
+  }
+  HIPCHK(hipGetLastError());
+  return WAR_OK;
+}
+
+AttnArgs attn_args(war_model* m, war_kv_pool* p, int TB, int chunk) {
+  AttnArgs a{};
+  a.q = m->q.as<bf16_t>();
+  a.q_stride = m->md.nq * m->md.hd;
+  a.kv = p->geom;
+  a.table = p->dev.table;
+  a.max_pages = p->dev.max_pages;
+  a.meta = m->meta();
+  a.G = m->md.nq / m->md.nkv;
+  a.TB = TB;
+  a.chunk = chunk;
+  a.n_kv_heads = m->md.nkv;
+  a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)m->md.hd));
+  a.pm = m->pm.as<float>();
+  a.pl = m->pl.as<float>();
+  a.po = m->po.as<float>();
+  a.o = m->o.as<bf16_t>();
+  return a;
+}
+
+war_status ensure_items(war_model* m, int64_t n_items, int RB) {
+  HIPCHK(m->items.ensure(std::max<int64_t>(n_items, 1) * sizeof(int4)));
+  const int64_t pr = std::max<int64_t>(n_items, 1) * m->md.nkv * RB;
+  HIPCHK(m->pm.ensure(pr * sizeof(float)));
+  HIPCHK(m->pl.ensure(pr * sizeof(float)));
+  HIPCHK(m->po.ensure(pr * m->md.hd * sizeof(float)));
+  return WAR_OK;
+}
+
+// Read the pool's device scalars (syncs the stream).
+war_status read_free_count(war_kv_pool* p, hipStream_t st, int32_t* fc, int32_t* err) {
+  int32_t sc[2];
+  HIPCHK(hipMemcpyAsync(sc, p->dev.scalars, sizeof(sc), hipMemcpyDeviceToHost, st));
+  HIPCHK(hipStreamSynchronize(st));
+  *fc = sc[0];
+  if (err) *err = sc[1];
+  p->free_lb = sc[0];
+  return WAR_OK;
+}
+
+war_status upload_ids(war_kv_pool* p, int n, const int32_t* a, const int32_t* b, hipStream_t st) {
+  HIPCHK(ensure_pinned(p->pinned, p->pinned_ints, 2 * (size_t)n));
+  HIPCHK(p->tmp.ensure(2 * (size_t)std::max(n, 1) * sizeof(int32_t)));
+  std::memcpy(p->pinned, a, n * sizeof(int32_t));
+  if (b) std::memcpy(p->pinned + n, b, n * sizeof(int32_t));
+  HIPCHK(hipMemcpyAsync(p->tmp.p, p->pinned, (b ? 2 : 1) * n * sizeof(int32_t), hipMemcpyHostToDevice, st));
+  return WAR_OK;
+}
+
+war_status check_ids(const war_kv_pool* p, int n, const int32_t* ids) {
+  std::unordered_set<int32_t> seen;
+  for (int i = 0; i < n; ++i) {
+    if (ids[i] < 0 || ids[i] >= p->dev.max_seqs) return fail(WAR_ERR_INVALID_ARG, "sequence id out of range");
+    if (!seen.insert(ids[i]).second) return fail(WAR_ERR_INVALID_ARG, "duplicate sequence id");
+  }
+  return WAR_OK;
+}
+
+}  // namespace
+
+// ===================================================================== C ABI
+extern "C" {
+
+const char* war_last_error(void) { return g_err.c_str(); }
+
+int32_t war_weight_count(const war_model_config* cfg) { return cfg ? 3 + 7 * cfg->n_layers : -1; }
+
+war_status war_model_create(const war_model_config* cfg, const void* const* weights, int32_t n_weights,
+                            war_model** out) {
+  if (!out) return fail(WAR_ERR_INVALID_ARG, "null out");
+  *out = nullptr;
+  war_status st = check_config(cfg);
+  if (st != WAR_OK) return st;
+  if (!weights || n_weights != war_weight_count(cfg))
+    return fail(WAR_ERR_INVALID_ARG, "expected 3 + 7*n_layers weight pointers");
+  for (int i = 0; i < n_weights; ++i)
+    if (!weights[i] || !aligned16(weights[i])) return fail(WAR_ERR_INVALID_ARG, "null or unaligned weight");
+  war_model* m = new war_model();
+  m->cfg = *cfg;
+  ModelDims& md = m->md;
+  md.d = cfg->d_model;
+  md.nq = cfg->n_q_heads;
+  md.nkv = cfg->n_kv_heads;
+  md.hd = cfg->head_dim;
+  md.F = cfg->ffn_dim;
+  md.V = cfg->vocab;
+  md.qkv = (md.nq + 2 * md.nkv) * md.hd;
+  md.eps = cfg->rms_eps;
+  int k = 0;
+  auto W = [&]() { return static_cast<const bf16_t*>(weights[k++]); };
+  m->embed = W();
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    LayerW L;
+    L.attn_norm = W();
+    L.w_qkv = W();
+    L.w_o = W();
+    L.ffn_norm = W();
+    L.w_gate = W();
+    L.w_up = W();
+    L.w_down = W();
+    m->layers.push_back(L);
+  }
+  m->final_norm = W();
+  m->w_lm = W();
+  const int R = cfg->max_rows;
+  m->max_rows = R;
+  m->n_req_cap = std::max(R, kMaxBatch);
+  m->n_seg_cap = R + kMaxBatch;
+  const size_t wide = std::max({md.d, md.F, md.nq * md.hd});
+  hipError_t e = hipSuccess;
+  auto ok = [&](hipError_t x) { if (e == hipSuccess) e = x; };
+  ok(m->h.ensure((size_t)R * md.d * 4));
+  ok(m->u.ensure((size_t)R * wide * 2));
+  ok(m->q.ensure((size_t)R * md.nq * md.hd * 2));
+  ok(m->o.ensure((size_t)R * md.nq * md.hd * 2));
+  const int64_t pneed = std::max<int64_t>((int64_t)R * std::max(md.qkv, 2 * md.F), 1);
+  ok(m->P.ensure((size_t)std::max(kPartialCap, pneed) * 4));
+  ok(m->cos_t.ensure((size_t)R * md.hd / 2 * 4));
+  ok(m->sin_t.ensure((size_t)R * md.hd / 2 * 4));
+  ok(m->inv_freq.ensure((size_t)md.hd / 2 * 8));
+  ok(m->amax_v.ensure((size_t)R * (md.V / 128) * 4));
+  ok(m->amax_i.ensure((size_t)R * (md.V / 128) * 4));
+  ok(m->rows_i32.ensure((size_t)4 * R * 4));
+  ok(m->reqs_i32.ensure((size_t)4 * m->n_req_cap * 4));
+  ok(m->segs_i32.ensure((size_t)4 * m->n_seg_cap * 4));
+  ok(m->n_items.ensure(16));
+  ok(m->a_rows.ensure((size_t)kMaxBatch * 4));
+  if (e == hipSuccess) {
+    std::vector<double> inv(md.hd / 2);
+    for (int j = 0; j < md.hd / 2; ++j) inv[j] = std::pow((double)cfg->rope_base, -2.0 * j / md.hd);
+    e = hipMemcpy(m->inv_freq.p, inv.data(), inv.size() * 8, hipMemcpyHostToDevice);
+  }
+  if (e != hipSuccess) {
+    war_model_destroy(m);
+    return fail(WAR_ERR_HIP, std::string("workspace allocation: ") + hipGetErrorString(e));
+  }
+  *out = m;
+  return WAR_OK;
+}
+
+void war_model_destroy(war_model* m) {
+  if (!m) return;
+  for (DevBuf* b : {&m->h, &m->u, &m->q, &m->o, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
+                    &m->amax_v, &m->amax_i, &m->rows_i32, &m->reqs_i32, &m->segs_i32, &m->n_items,
+                    &m->items, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
+    b->release();
+  if (m->pinned) (void)hipHostFree(m->pinned);
+  delete m;
+}
+
+war_status war_kv_pool_create(const war_model_config* cfg, void* kv_pages, int32_t num_pages,
+                              int32_t* block_tables, int32_t max_seqs, int32_t max_pages_per_seq,
+                              void* stream, war_kv_pool** out) {
+  if (!out) return fail(WAR_ERR_INVALID_ARG, "null out");
+  *out = nullptr;
+  war_status s0 = check_config(cfg);
+  if (s0 != WAR_OK) return s0;
+  CHECK(kv_pages && block_tables, "null kv_pages or block_tables");
+  CHECK(aligned16(kv_pages), "kv_pages must be 16-byte aligned");
+  CHECK(num_pages > 0 && max_seqs > 0 && max_pages_per_seq > 0, "non-positive pool size");
+  CHECK((int64_t)max_pages_per_seq * cfg->page_size <= (1 << 24), "max_pages_per_seq too large");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  war_kv_pool* p = new war_kv_pool();
+  p->cfg = *cfg;
+  p->geom.kv = static_cast<bf16_t*>(kv_pages);
+  p->geom.num_pages = num_pages;
+  p->geom.n_kv_heads = cfg->n_kv_heads;
+  p->geom.head_dim = cfg->head_dim;
+  p->geom.page_size = cfg->page_size;
+  const size_t words = (size_t)2 * num_pages + 2 * (size_t)max_seqs + 4;
+  hipError_t e = p->state.ensure(words * 4);
+  if (e != hipSuccess) {
+    delete p;
+    return fail(WAR_ERR_HIP, std::string("pool state allocation: ") + hipGetErrorString(e));
+  }
+  int32_t* w = p->state.as<int32_t>();
+  p->dev.stack = w;
+  p->dev.refcount = w + num_pages;
+  p->dev.held = w + 2 * (size_t)num_pages;
+  p->dev.base = p->dev.held + max_seqs;
+  p->dev.scalars = p->dev.base + max_seqs;
+  p->dev.table = block_tables;
+  p->dev.num_pages = num_pages;
+  p->dev.max_seqs = max_seqs;
+  p->dev.max_pages = max_pages_per_seq;
+  p->dev.page_size = cfg->page_size;
+  p->free_lb = num_pages;
+  launch_pool_init(p->dev, st);
+  e = hipGetLastError();
+  if (e != hipSuccess) {
+    war_kv_pool_destroy(p);
+    return fail(WAR_ERR_HIP, std::string("pool init: ") + hipGetErrorString(e));
+  }
+  *out = p;
+  return WAR_OK;
+}
+
+void war_kv_pool_destroy(war_kv_pool* p) {
+  if (!p) return;
+  p->state.release();
+  p->tmp.release();
+  if (p->pinned) (void)hipHostFree(p->pinned);
+  delete p;
+}
+
+war_status war_pool_state(war_kv_pool* p, int32_t* free_count, int32_t* free_stack, int32_t* refcount,
+                          int32_t* held, int32_t* step_base, void* stream) {
+  CHECK(p, "null pool");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t fc, err;
+  war_status s = read_free_count(p, st, &fc, &err);
+  if (s != WAR_OK) return s;
+  if (free_count) *free_count = fc;
+  if (free_stack) HIPCHK(hipMemcpy(free_stack, p->dev.stack, (size_t)p->dev.num_pages * 4, hipMemcpyDeviceToHost));
+  if (refcount) HIPCHK(hipMemcpy(refcount, p->dev.refcount, (size_t)p->dev.num_pages * 4, hipMemcpyDeviceToHost));
+  if (held) HIPCHK(hipMemcpy(held, p->dev.held, (size_t)p->dev.max_seqs * 4, hipMemcpyDeviceToHost));
+  if (step_base) HIPCHK(hipMemcpy(step_base, p->dev.base, (size_t)p->dev.max_seqs * 4, hipMemcpyDeviceToHost));
+  if (err) return fail(WAR_ERR_DEVICE, err & ERR_NO_PAGES ? "device page shortage" : "bad token id or context length on device");
+  return WAR_OK;
+}
+
+war_status war_kv_alloc(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host, const int32_t* n_tokens_host,
+                        void* stream) {
+  CHECK(p, "null pool");
+  CHECK(!p->pending, "a verify step is waiting for war_kv_commit");
+  CHECK(n >= 0 && n <= kMaxBatch, "n out of range [0, 1024]");
+  if (n == 0) return WAR_OK;
+  CHECK(seq_ids_host && n_tokens_host, "null array");
+  war_status s = check_ids(p, n, seq_ids_host);
+  if (s != WAR_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int64_t bound = 0;
+  for (int i = 0; i < n; ++i) {
+    CHECK(n_tokens_host[i] >= 0, "negative token count");
+    const int pg = cdiv_i(n_tokens_host[i], p->dev.page_size);
+    CHECK(pg <= p->dev.max_pages, "n_tokens exceeds max_pages_per_seq");
+    bound += pg;
+  }
+  int64_t need = bound;
+  if (bound > p->free_lb) {
+    int32_t fc;
+    s = read_free_count(p, st, &fc, nullptr);
+    if (s != WAR_OK) return s;
+    std::vector<int32_t> held(p->dev.max_seqs);
+    HIPCHK(hipMemcpy(held.data(), p->dev.held, held.size() * 4, hipMemcpyDeviceToHost));
+    need = 0;
+    for (int i = 0; i < n; ++i)
+      need += std::max(0, cdiv_i(n_tokens_host[i], p->dev.page_size) - held[seq_ids_host[i]]);
+    if (need > fc) return fail(WAR_ERR_OUT_OF_PAGES, "not enough free KV pages");
+  }
+  s = upload_ids(p, n, seq_ids_host, n_tokens_host, st);
+  if (s != WAR_OK) return s;
+  const int32_t* d = p->tmp.as<int32_t>();
+  launch_grow(p->dev, n, d, d + n, nullptr, 0, st);
+  HIPCHK(hipGetLastError());
+  HIPCHK(hipStreamSynchronize(st));  // the pinned staging buffer is reused
+  p->free_lb -= need;
+  return WAR_OK;
+}
+
+war_status war_kv_fork(war_kv_pool* p, int32_t src_seq, int32_t dst_seq, int32_t n_tokens, void* stream) {
+  CHECK(p, "null pool");
+  CHECK(!p->pending, "a verify step is waiting for war_kv_commit");
+  CHECK(src_seq >= 0 && src_seq < p->dev.max_seqs && dst_seq >= 0 && dst_seq < p->dev.max_seqs &&
+            src_seq != dst_seq, "bad sequence ids");
+  CHECK(n_tokens >= 0 && n_tokens % p->dev.page_size == 0, "fork length must be a multiple of the page size");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t hs, hd;
+  HIPCHK(hipMemcpyAsync(&hs, p->dev.held + src_seq, 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipMemcpyAsync(&hd, p->dev.held + dst_seq, 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipStreamSynchronize(st));
+  const int npg = n_tokens / p->dev.page_size;
+  CHECK(hd == 0, "fork destination already holds pages");
+  CHECK(hs >= npg, "fork source holds fewer pages");
+  launch_fork(p->dev, src_seq, dst_seq, npg, st);
+  HIPCHK(hipGetLastError());
+  return WAR_OK;
+}
+
+war_status war_kv_free(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host, void* stream) {
+  CHECK(p, "null pool");
+  CHECK(!p->pending, "a verify step is waiting for war_kv_commit");
+  CHECK(n >= 0 && n <= kMaxBatch, "n out of range [0, 1024]");
+  if (n == 0) return WAR_OK;
+  CHECK(seq_ids_host, "null array");
+  war_status s = check_ids(p, n, seq_ids_host);
+  if (s != WAR_OK) return s;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  s = upload_ids(p, n, seq_ids_host, nullptr, st);
+  if (s != WAR_OK) return s;
+  launch_free(p->dev, n, p->tmp.as<int32_t>(), st);
+  HIPCHK(hipGetLastError());
+  HIPCHK(hipStreamSynchronize(st));
+  return WAR_OK;
+}
+
+war_status war_kv_load(war_kv_pool* p, int32_t seq_id, int32_t layer, int32_t pos0, int32_t n,
+                       const void* src, void* stream) {
+  CHECK(p && src, "null pool or src");
+  CHECK(seq_id >= 0 && seq_id < p->dev.max_seqs, "sequence id out of range");
+  CHECK(layer >= 0 && layer < p->cfg.n_layers, "layer out of range");
+  CHECK(pos0 >= 0 && n >= 0, "negative position or count");
+  if (n == 0) return WAR_OK;
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  int32_t hs;
+  HIPCHK(hipMemcpyAsync(&hs, p->dev.held + seq_id, 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipStreamSynchronize(st));
+  CHECK((int64_t)pos0 + n <= (int64_t)hs * p->dev.page_size, "tokens beyond the sequence's pages");
+  launch_kv_load(p->dev, p->geom, seq_id, layer, pos0, n, static_cast<const bf16_t*>(src), st);
+  HIPCHK(hipGetLastError());
+  return WAR_OK;
+}
+
+war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                           const int32_t* ctx_lens, const int32_t* last_tokens, const int32_t* draft_tokens,
+                           const int32_t* draft_lens, int32_t k_max, int32_t* accept_lens,
+                           int32_t* next_tokens, float* logits, void* stream) {
+  CHECK(m && p, "null model or pool");
+  CHECK(same_shape(m->cfg, p->cfg), "model and pool shapes differ");
+  CHECK(!p->pending, "previous verify step not committed");
+  CHECK(B >= 1 && B <= kMaxBatch && B <= p->dev.max_seqs, "B out of range");
+  CHECK(k_max >= 0, "negative k_max");
+  const int G = m->md.nq / m->md.nkv;
+  if (G * (k_max + 1) > 48) return fail(WAR_ERR_UNSUPPORTED, "n_q/n_kv * (k_max+1) must be <= 48");
+  CHECK((int64_t)B * (k_max + 1) <= m->max_rows, "B*(k_max+1) exceeds max_rows");
+  CHECK(seq_ids && ctx_lens && last_tokens && accept_lens && next_tokens, "null array");
+  CHECK(k_max == 0 || draft_tokens, "draft_tokens required when k_max > 0");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int P = p->dev.page_size;
+
+  // capacity: ctx + draft + 1 slots need at most cdiv(k_max+1, P) new pages per request
+  const int64_t bound = (int64_t)B * cdiv_i(k_max + 1, P);
+  int64_t need = bound;
+  if (bound > p->free_lb) {
+    int32_t fc;
+    war_status s = read_free_count(p, st, &fc, nullptr);
+    if (s != WAR_OK) return s;
+    if (bound > fc) {
+      std::vector<int32_t> sid(B), ctx(B), dl(B, k_max), held(p->dev.max_seqs);
+      HIPCHK(hipMemcpy(sid.data(), seq_ids, B * 4, hipMemcpyDeviceToHost));
+      HIPCHK(hipMemcpy(ctx.data(), ctx_lens, B * 4, hipMemcpyDeviceToHost));
+      if (draft_lens) HIPCHK(hipMemcpy(dl.data(), draft_lens, B * 4, hipMemcpyDeviceToHost));
+      HIPCHK(hipMemcpy(held.data(), p->dev.held, held.size() * 4, hipMemcpyDeviceToHost));
+      need = 0;
+      for (int b = 0; b < B; ++b) {
+        CHECK(sid[b] >= 0 && sid[b] < p->dev.max_seqs, "sequence id out of range");
+        const int d = std::min(std::max(dl[b], 0), k_max);
+        need += std::max(0, cdiv_i(std::max(ctx[b], 0) + d + 1, P) - held[sid[b]]);
+      }
+      if (need > fc) return fail(WAR_ERR_OUT_OF_PAGES, "not enough free KV pages for the draft slots");
+    }
+  }
+
+  const int kp1 = k_max + 1;
+  const int R = B * kp1;
+  const int RB = attn_rows_per_block(G, kp1);
+  int chunk = 256;
+  while (chunk < 2048 && chunk * 2 <= G * kp1 * 32) chunk *= 2;
+  const int64_t max_items = (int64_t)B * cdiv_i(p->dev.max_pages * P, chunk);
+  war_status s = ensure_items(m, max_items, RB);
+  if (s != WAR_OK) return s;
+
+  VerifySetupArgs va;
+  va.B = B;
+  va.k_max = k_max;
+  va.vocab = m->md.V;
+  va.chunk = chunk;
+  va.seq_ids = seq_ids;
+  va.ctx_lens = ctx_lens;
+  va.last_tokens = last_tokens;
+  va.draft_tokens = draft_tokens;
+  va.draft_lens = draft_lens;
+  launch_verify_setup(p->dev, va, m->meta(), st);
+
+  AttnArgs a = attn_args(m, p, kp1, chunk);
+  const int grid = (int)std::min<int64_t>(max_items * m->md.nkv, RB == 48 ? 1024 : 2048);
+  s = run_layers(m, p, R, a, RB, grid, B, st);
+  if (s != WAR_OK) return s;
+  int sdummy;
+  gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, nullptr, 0, R, m->md.V, m->md.d, &sdummy, st,
+       true, logits);
+  launch_argmax_accept(B, m->meta().req_ntok, kp1, m->md.V / 128, m->amax_v.as<float>(),
+                       m->amax_i.as<int32_t>(), draft_tokens, k_max, accept_lens, next_tokens, st);
+  HIPCHK(hipGetLastError());
+  p->free_lb -= need;
+  p->pending = true;
+  p->pending_B = B;
+  return WAR_OK;
+}
+
+war_status war_kv_commit(war_kv_pool* p, int32_t B, const int32_t* seq_ids, int32_t* ctx_lens,
+                         const int32_t* accept_lens, void* stream) {
+  CHECK(p, "null pool");
+  CHECK(p->pending, "no verify step to commit");
+  CHECK(B == p->pending_B, "B differs from the verify step's");
+  CHECK(seq_ids && ctx_lens && accept_lens, "null array");
+  launch_commit(p->dev, B, seq_ids, ctx_lens, accept_lens, static_cast<hipStream_t>(stream));
+  HIPCHK(hipGetLastError());
+  p->pending = false;
+  return WAR_OK;
+}
+
+war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int32_t* seq_ids,
+                              int32_t* ctx_lens, const int32_t* n_new_host, const int32_t* new_tokens,
+                              int32_t* next_tokens, float* last_logits, void* stream) {
+  CHECK(m && p, "null model or pool");
+  CHECK(same_shape(m->cfg, p->cfg), "model and pool shapes differ");
+  CHECK(!p->pending, "a verify step is waiting for war_kv_commit");
+  CHECK(n >= 1 && n <= kMaxBatch, "n out of range [1, 1024]");
+  CHECK(seq_ids && ctx_lens && n_new_host && new_tokens && next_tokens, "null array");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  const int P = p->dev.page_size;
+  const int G = m->md.nq / m->md.nkv;
+  int64_t total = 0;
+  for (int i = 0; i < n; ++i) {
+    CHECK(n_new_host[i] >= 1, "n_new must be >= 1");
+    total += n_new_host[i];
+  }
+  CHECK(total <= (int64_t)1 << 30, "too many new tokens");
+  // read ids, lengths and held pages (one synchronisation)
+  std::vector<int32_t> sid(n), ctx(n), held(p->dev.max_seqs), toks(total);
+  HIPCHK(hipMemcpyAsync(toks.data(), new_tokens, total * 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipMemcpyAsync(sid.data(), seq_ids, n * 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipMemcpyAsync(ctx.data(), ctx_lens, n * 4, hipMemcpyDeviceToHost, st));
+  HIPCHK(hipMemcpyAsync(held.data(), p->dev.held, held.size() * 4, hipMemcpyDeviceToHost, st));
+  int32_t fc;
+  war_status s = read_free_count(p, st, &fc, nullptr);
+  if (s != WAR_OK) return s;
+  s = check_ids(p, n, sid.data());
+  if (s != WAR_OK) return s;
+  for (int64_t i = 0; i < total; ++i)
+    CHECK(toks[i] >= 0 && toks[i] < m->md.V, "token id outside [0, vocab)");
+  int64_t need = 0;
+  for (int i = 0; i < n; ++i) {
+    CHECK(ctx[i] >= 0, "negative ctx_len");
+    const int64_t pages = cdiv_i(ctx[i] + n_new_host[i], P);
+    CHECK(pages <= p->dev.max_pages, "sequence would exceed max_pages_per_seq");
+    CHECK(ctx[i] <= (int64_t)held[sid[i]] * P, "ctx_len beyond the sequence's pages");
+    need += std::max<int64_t>(0, pages - held[sid[i]]);
+  }
+  if (need > fc) return fail(WAR_ERR_OUT_OF_PAGES, "not enough free KV pages for the new tokens");
+
+  // reserve: targets = ctx + n_new
+  HIPCHK(m->stage_dev.ensure((size_t)n * 4));
+  HIPCHK(ensure_pinned(m->pinned, m->pinned_ints, (size_t)n));
+  std::memcpy(m->pinned, n_new_host, n * 4);
+  int32_t* d_new = m->stage_dev.as<int32_t>();
+  HIPCHK(hipMemcpyAsync(d_new, m->pinned, n * 4, hipMemcpyHostToDevice, st));
+  launch_grow(p->dev, n, seq_ids, ctx_lens, d_new, 1, st);
+  HIPCHK(hipGetLastError());
+  p->free_lb = fc - need;
+
+  // forward over chunks of at most max_rows packed rows
+  const int RB = 48;
+  const int TB = RB / G;
+  const int chunk = kPrefillChunk;
+  std::vector<int64_t> cu(n + 1, 0);
+  for (int i = 0; i < n; ++i) cu[i + 1] = cu[i] + n_new_host[i];
+  const int R_cap = m->max_rows;
+  for (int64_t r0 = 0; r0 < total; r0 += R_cap) {
+    const int64_t r1 = std::min<int64_t>(total, r0 + R_cap);
+    const int R = (int)(r1 - r0);
+    // requests of this chunk
+    std::vector<int32_t> rq_seq, rq_pos0, rq_ntok, rq_row0, rq_idx;
+    for (int i = 0; i < n; ++i) {
+      const int64_t a = std::max<int64_t>(r0, cu[i]), b = std::min<int64_t>(r1, cu[i + 1]);
+      if (a >= b) continue;
+      rq_idx.push_back(i);
+      rq_seq.push_back(sid[i]);
+      rq_pos0.push_back((int32_t)(ctx[i] + (a - cu[i])));
+      rq_ntok.push_back((int32_t)(b - a));
+      rq_row0.push_back((int32_t)(a - r0));
+    }
+    const int nr = (int)rq_seq.size();
+    std::vector<int32_t> pos(R), act(R, 1), rreq(R);
+    std::vector<int32_t> sg_b, sg_c, sg_r, sg_rb;
+    std::vector<int4> items;
+    for (int j = 0; j < nr; ++j) {
+      for (int t = 0; t < rq_ntok[j]; ++t) {
+        pos[rq_row0[j] + t] = rq_pos0[j] + t;
+        rreq[rq_row0[j] + t] = j;
+      }
+      for (int rb = 0; rb * TB < rq_ntok[j]; ++rb) {
+        const int S = rq_pos0[j] + std::min(rq_ntok[j], (rb + 1) * TB);
+        const int nch = cdiv_i(S, chunk);
+        sg_b.push_back((int32_t)items.size());
+        sg_c.push_back(nch);
+        sg_r.push_back(j);
+        sg_rb.push_back(rb);
+        for (int c = 0; c < nch; ++c) items.push_back(make_int4(j, rb, c, 0));
+      }
+    }
+    const int nseg = (int)sg_b.size();
+    CHECK(nseg <= m->n_seg_cap && nr <= m->n_req_cap, "internal: prefill chunk too fragmented");
+    // previous chunk's kernels read the metadata buffers: wait before overwriting
+    // (and before ensure_items may reallocate the work list)
+    HIPCHK(hipStreamSynchronize(st));
+    s = ensure_items(m, (int64_t)items.size(), RB);
+    if (s != WAR_OK) return s;
+    const StepMeta meta = m->meta();  // after any reallocation
+    auto h2d = [&](void* dst, const void* src, size_t bytes) {
+      return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, st);
+    };
+    HIPCHK(h2d(meta.pos, pos.data(), R * 4));
+    HIPCHK(h2d(meta.active, act.data(), R * 4));
+    HIPCHK(h2d(meta.row_req, rreq.data(), R * 4));
+    HIPCHK(hipMemcpyAsync(meta.tok, new_tokens + r0, R * 4, hipMemcpyDeviceToDevice, st));
+    HIPCHK(h2d(meta.req_seq, rq_seq.data(), nr * 4));
+    HIPCHK(h2d(meta.req_pos0, rq_pos0.data(), nr * 4));
+    HIPCHK(h2d(meta.req_ntok, rq_ntok.data(), nr * 4));
+    HIPCHK(h2d(meta.req_row0, rq_row0.data(), nr * 4));
+    HIPCHK(h2d(meta.seg_begin, sg_b.data(), nseg * 4));
+    HIPCHK(h2d(meta.seg_count, sg_c.data(), nseg * 4));
+    HIPCHK(h2d(meta.seg_req, sg_r.data(), nseg * 4));
+    HIPCHK(h2d(meta.seg_rb, sg_rb.data(), nseg * 4));
+    HIPCHK(h2d(meta.items, items.data(), items.size() * sizeof(int4)));
+    const int32_t ni = (int32_t)items.size();
+    HIPCHK(h2d(meta.n_items, &ni, 4));
+    HIPCHK(hipStreamSynchronize(st));  // host vectors go out of scope below
+
+    AttnArgs a = attn_args(m, p, TB, chunk);
+    const int grid = (int)std::min<int64_t>((int64_t)ni * m->md.nkv, 2048);
+    s = run_layers(m, p, R, a, RB, std::max(grid, 1), nseg, st);
+    if (s != WAR_OK) return s;
+    // LM head on the rows that end a sequence inside this chunk
+    std::vector<int32_t> last_rows;
+    int first_seq = -1;
+    for (int j = 0; j < nr; ++j) {
+      const int i = rq_idx[j];
+      if (cu[i + 1] <= r1 && cu[i + 1] > r0) {
+        if (first_seq < 0) first_seq = i;
+        last_rows.push_back((int32_t)(cu[i + 1] - 1 - r0));
+      }
+    }
+    if (!last_rows.empty()) {
+      const int nl = (int)last_rows.size();
+      HIPCHK(hipMemcpyAsync(m->a_rows.p, last_rows.data(), nl * 4, hipMemcpyHostToDevice, st));
+      int sd;
+      gemm(m, m->u.as<bf16_t>(), m->md.d, m->a_rows.as<int32_t>(), m->w_lm, nullptr, 0, nl, m->md.V,
+           m->md.d, &sd, st, true, last_logits ? last_logits + (int64_t)first_seq * m->md.V : nullptr);
+      launch_argmax_accept(nl, nullptr, 1, m->md.V / 128, m->amax_v.as<float>(), m->amax_i.as<int32_t>(),
+                           nullptr, 0, nullptr, next_tokens + first_seq, st);
+      HIPCHK(hipGetLastError());
+      HIPCHK(hipStreamSynchronize(st));  // last_rows goes out of scope
+    }
+  }
+  launch_add_ctx(n, ctx_lens, d_new, st);
+  HIPCHK(hipGetLastError());
+  HIPCHK(hipStreamSynchronize(st));
+  return WAR_OK;
+}
+
+war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes) {
+  CHECK(m && name && ptr && bytes, "null argument");
+  const std::string n(name);
+  const DevBuf* b = n == "h" ? &m->h : n == "u" ? &m->u : n == "q" ? &m->q : n == "o" ? &m->o
+                  : n == "P" ? &m->P : n == "pm" ? &m->pm : n == "pl" ? &m->pl : n == "po" ? &m->po
+                  : n == "rows" ? &m->rows_i32 : n == "reqs" ? &m->reqs_i32 : n == "items" ? &m->items
+                  : nullptr;
+  CHECK(b, "unknown workspace buffer");
+  *ptr = b->p;
+  *bytes = (int64_t)b->bytes;
+  return WAR_OK;
+}
+
+}  // extern "C"

@@ -202,24 +202,27 @@ def weight_shapes(cfg: ModelConfig) -> List[Tuple[str, Tuple[int, ...]]]:
 
 
 def make_weight(cfg: ModelConfig, seed: int, index: int, name: str, shape, device="cpu",
-                norm_std: float = 0.0) -> torch.Tensor:
+                norm_std: float = 0.0, lm_std: float = WEIGHT_STD) -> torch.Tensor:
     numel = int(np.prod(shape))
     key = stream_key(seed, index)
     if name.endswith("norm"):
         if norm_std == 0.0:
             return torch.ones(shape, dtype=torch.bfloat16, device=device)
         return (1.0 + normalish(key, numel, norm_std, device).float()).to(torch.bfloat16).view(shape)
-    return normalish(key, numel, WEIGHT_STD, device).view(shape)
+    std = lm_std if name == "w_lm" else WEIGHT_STD
+    return normalish(key, numel, std, device).view(shape)
 
 
-def model_weights(cfg: ModelConfig, seed: int, device="cpu", norm_std: float = 0.0
-                  ) -> Dict[str, torch.Tensor]:
+def model_weights(cfg: ModelConfig, seed: int, device="cpu", norm_std: float = 0.0,
+                  lm_std: float = WEIGHT_STD) -> Dict[str, torch.Tensor]:
     """All weights of the decoder, bf16, in canonical order (dict keeps order).
 
     Matrices are approximately N(0, 0.02); norm gains are 1 (or 1 + N(0, norm_std)
-    when ``norm_std`` > 0, used by tests to make the gains matter).
+    when ``norm_std`` > 0, used by tests to make the gains matter).  ``lm_std``
+    rescales the LM head (tests use a larger value so that the top two logits
+    of a row are rarely within rounding distance of each other).
     """
-    return {name: make_weight(cfg, seed, i, name, shape, device, norm_std)
+    return {name: make_weight(cfg, seed, i, name, shape, device, norm_std, lm_std)
             for i, (name, shape) in enumerate(weight_shapes(cfg))}
 
 

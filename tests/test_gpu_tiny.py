@@ -1,0 +1,295 @@
+"""GPU parity on the tiny decoder (2 layers, d 256, 4/2 heads, vocab 4096):
+matrix-core lane layout, input generators CPU == GPU, paged-KV bookkeeping
+bit-exact against the oracle pool, and the whole prefill -> verify -> commit
+path against the oracle (logits, accept lengths, next tokens, KV contents)."""
+import copy
+
+import numpy as np
+import pytest
+import torch
+
+from oracle.accept import argmax_lowest
+from oracle.decoder import RequestKV, Weights
+from oracle.pages import PagePool
+from oracle.verify import commit_request, greedy_decode, prefill_request, verify_request
+from paper_2607_17299_amd import synth
+from paper_2607_17299_amd.drafter import SuffixDrafter
+from parity import compare_request
+
+pytestmark = pytest.mark.gpu
+CFG = synth.TINY
+DEV = "cuda"
+
+
+def _war():
+    from paper_2607_17299_amd import war
+    return war
+
+
+def test_mfma_lane_layout():
+    war = _war()
+    g = torch.Generator().manual_seed(0)
+    A = torch.randn(16, 32, generator=g).to(torch.bfloat16)
+    B = torch.randn(32, 16, generator=g).to(torch.bfloat16)
+    C = war.debug_mfma16(A.to(DEV), B.to(DEV)).cpu()
+    ref = A.double() @ B.double()
+    assert torch.allclose(C.double(), ref, atol=1e-4, rtol=1e-5), (C.double() - ref).abs().max()
+
+
+def test_generators_identical_on_cpu_and_gpu():
+    for shape_cfg, seed in ((CFG, 0), (synth.reduced(synth.LARGE, 1, vocab=1024), 1)):
+        for i, (name, shape) in enumerate(synth.weight_shapes(shape_cfg)[:6]):
+            a = synth.make_weight(shape_cfg, seed, i, name, shape, "cpu", norm_std=0.1)
+            b = synth.make_weight(shape_cfg, seed, i, name, shape, DEV, norm_std=0.1).cpu()
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), name
+    a = synth.kv_context(synth.LARGE, 5, 3, 7, 1000, 300, "cpu")
+    b = synth.kv_context(synth.LARGE, 5, 3, 7, 1000, 300, DEV).cpu()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+# --------------------------------------------------------------------------- setup
+@pytest.fixture(scope="module")
+def tiny():
+    war = _war()
+    w_cpu = synth.model_weights(CFG, seed=0, norm_std=0.1)
+    w_gpu = {k: v.to(DEV) for k, v in w_cpu.items()}
+    model = war.Model(CFG, w_gpu, max_rows=256)
+    return {"war": war, "w_cpu": w_cpu, "W": Weights(CFG, w_cpu), "model": model, "w_gpu": w_gpu}
+
+
+def _snap_equal(gpu_state, oracle: PagePool, tag=""):
+    o = oracle.snapshot()
+    np.testing.assert_array_equal(gpu_state["stack"], o["stack"], err_msg=tag + " stack")
+    np.testing.assert_array_equal(gpu_state["refcount"], o["refcount"], err_msg=tag + " refcount")
+    np.testing.assert_array_equal(gpu_state["held"], o["held"], err_msg=tag + " held")
+    np.testing.assert_array_equal(gpu_state["base"], o["base"], err_msg=tag + " base")
+    np.testing.assert_array_equal(gpu_state["table"], o["table"], err_msg=tag + " table")
+
+
+def test_bookkeeping_bit_exact_against_oracle(tiny):
+    war, model = tiny["war"], tiny["model"]
+    rng = np.random.default_rng(0)
+    NP, S, MP = 96, 6, 24
+    pool = war.Pool(CFG, NP, S, MP)
+    ora = PagePool(NP, 16, S, MP)
+    ctx = np.zeros(S, np.int64)
+    st = pool.state()
+    assert st["status"] == 0
+    _snap_equal(st, ora, "init")
+    for step in range(40):
+        op = int(rng.integers(0, 5))
+        ids = rng.permutation(S)[: int(rng.integers(1, S + 1))].tolist()
+        tag = f"step {step} op {op}"
+        if op == 0:
+            n = [int(x) for x in rng.integers(0, 120, len(ids))]
+            try:
+                ora.alloc(ids, n)
+            except Exception:
+                with pytest.raises(war.WarError):
+                    pool.alloc(ids, n)
+                continue
+            pool.alloc(ids, n)
+            for s in ids:
+                ctx[s] = min(ctx[s], int(ora.held[s]) * 16)
+        elif op == 1:
+            src, dst = int(rng.integers(S)), int(rng.integers(S))
+            n = int(rng.integers(0, ora.held[src] + 1)) * 16
+            try:
+                ora.fork(src, dst, n)
+            except Exception:
+                with pytest.raises(war.WarError):
+                    pool.fork(src, dst, n)
+                continue
+            pool.fork(src, dst, n)
+            ctx[dst] = n
+        elif op == 2:
+            ora.free(ids)
+            pool.free(ids)
+            ctx[ids] = 0
+        else:
+            # a verify step on the tiny model; commit with chosen accept lengths
+            k = int(rng.integers(0, 5))
+            dl = [int(x) for x in rng.integers(0, k + 1, len(ids))]
+            c = [int(ctx[s]) for s in ids]
+            try:
+                ora.reserve(ids, c, dl)
+            except Exception:
+                continue   # out of pages: covered by the capacity test
+            B = len(ids)
+            t = lambda a: torch.tensor(a, dtype=torch.int32, device=DEV)
+            drafts = t(rng.integers(0, CFG.vocab, (B, max(k, 1))).tolist())
+            acc, nxt = t([0] * B), t([0] * B)
+            war.verify_step(model, pool, t(ids), t(c), t(rng.integers(0, CFG.vocab, B).tolist()),
+                            drafts, t(dl), k, acc, nxt)
+            st = pool.state()
+            assert st["status"] == 0, tag
+            _snap_equal(st, ora, tag + " reserve")
+            choose = [int(rng.integers(-1, d + 1)) for d in dl]
+            ctx_d = t(c)
+            war.kv_commit(pool, t(ids), ctx_d, t(choose))
+            new = ora.commit(ids, c, choose)
+            np.testing.assert_array_equal(ctx_d.cpu().numpy(), new, err_msg=tag)
+            for s, v in zip(ids, new):
+                ctx[s] = int(v)
+        st = pool.state()
+        assert st["status"] == 0, tag
+        _snap_equal(st, ora, tag)
+        ora.check_invariants()
+
+
+def test_out_of_pages_is_reported_without_state_change(tiny):
+    war = tiny["war"]
+    pool = war.Pool(CFG, 8, 3, 8)
+    pool.alloc([0], [100])
+    before = pool.state()
+    with pytest.raises(war.WarError) as e:
+        pool.alloc([1], [64])
+    assert e.value.status == -2
+    after = pool.state()
+    for k in ("stack", "refcount", "held", "table"):
+        np.testing.assert_array_equal(before[k], after[k])
+
+
+# ------------------------------------------------------------- end-to-end parity
+def _tiny_workload(seed=1, B=4, ctx_len=512, k=4):
+    prior = [synth.uniform_tokens(100 + seed * 10 + i, 1024, CFG.vocab) for i in range(8)]
+    ctxs = [synth.uniform_tokens(200 + seed * 10 + b, ctx_len, CFG.vocab) for b in range(B)]
+    return prior, ctxs
+
+
+def _prefill_both(tiny, ctxs, pool_pages=256):
+    war, model, W = tiny["war"], tiny["model"], tiny["W"]
+    B = len(ctxs)
+    pool = war.Pool(CFG, pool_pages, B, 64)
+    seq = torch.arange(B, dtype=torch.int32, device=DEV)
+    ctx = torch.zeros(B, dtype=torch.int32, device=DEV)
+    toks = torch.from_numpy(np.concatenate(ctxs)).to(torch.int32).to(DEV)
+    nxt = torch.zeros(B, dtype=torch.int32, device=DEV)
+    last = torch.zeros((B, CFG.vocab), dtype=torch.float32, device=DEV)
+    war.prefill_append(model, pool, seq, ctx, [len(c) for c in ctxs], toks, nxt, last)
+    torch.cuda.synchronize()
+    kvs, onext, ologits = [], [], []
+    for c in ctxs:
+        kv = RequestKV(CFG)
+        r = prefill_request(CFG, W, kv, c)
+        kvs.append(kv)
+        onext.append(r["next"])
+        ologits.append(r["logits"][-1])
+    return pool, seq, ctx, kvs, np.array(onext), np.stack(ologits), nxt.cpu().numpy(), last.cpu().numpy()
+
+
+def test_prefill_matches_oracle(tiny):
+    _, ctxs = _tiny_workload(seed=1, B=3, ctx_len=300)
+    ctxs[1] = ctxs[1][:37]     # ragged: a partial page and a short sequence
+    pool, seq, ctx, kvs, onext, ologits, gnext, glogits = _prefill_both(tiny, ctxs)
+    assert ctx.cpu().tolist() == [len(c) for c in ctxs]
+    err = np.abs(glogits - ologits).max()
+    assert err < 5e-2, err
+    for b in range(len(ctxs)):
+        if gnext[b] != onext[b]:
+            gap = np.sort(ologits[b])[-1] - np.sort(ologits[b])[-2]
+            assert gap <= 2 * np.abs(glogits[b] - ologits[b]).max() + 1e-6
+        for l in range(CFG.n_layers):
+            g = pool.gather_kv(b, len(ctxs[b]), l).double().cpu().numpy()
+            K, V = kvs[b].get(l)
+            np.testing.assert_allclose(g[0], K, atol=2e-2, rtol=2e-2)
+            np.testing.assert_allclose(g[1], V, atol=2e-2, rtol=2e-2)
+
+
+def _run_steps(tiny, steps, draft_mode, seed, report):
+    """Prefill 4 x 512, then `steps` verify+commit steps with drafts from the
+    host suffix drafter ('suffix'), the oracle's own greedy continuation
+    ('greedy'), or a mix with corrupted positions ('mixed')."""
+    war, model, W = tiny["war"], tiny["model"], tiny["W"]
+    prior, ctxs = _tiny_workload(seed=seed)
+    B, k = len(ctxs), 4
+    pool, seq, ctx, kvs, onext, *_ = _prefill_both(tiny, ctxs)
+    drafter = SuffixDrafter()
+    for p in prior:
+        drafter.add_trajectory(p)
+    hist = [list(c) for c in ctxs]
+    pending = [int(x) for x in onext]          # inputs always come from the oracle side
+    rng = np.random.default_rng(seed)
+    stats = []
+    for step in range(steps):
+        drafts = []
+        for b in range(B):
+            if draft_mode == "suffix":
+                d = drafter.propose(hist[b] + [pending[b]], k)
+            else:
+                d = greedy_decode(CFG, W, copy.deepcopy(kvs[b]), pending[b], k)
+                if draft_mode == "mixed":
+                    d = [int(rng.integers(CFG.vocab)) if rng.random() < 0.3 else x for x in d]
+                d = d[: int(rng.integers(0, k + 1))] if draft_mode == "mixed" else d
+            drafts.append(d)
+        dl = [len(d) for d in drafts]
+        dt = np.zeros((B, k), np.int32)
+        for b, d in enumerate(drafts):
+            dt[b, : len(d)] = d
+        t = lambda a: torch.tensor(np.asarray(a), dtype=torch.int32, device=DEV)
+        acc, nxt = t([0] * B), t([0] * B)
+        logits = torch.full((B * (k + 1), CFG.vocab), float("nan"), device=DEV)
+        ctx_before = ctx.cpu().numpy().copy()
+        war.verify_step(model, pool, seq, ctx, t(pending), t(dt), t(dl), k, acc, nxt, logits)
+        war.kv_commit(pool, seq, ctx, acc)
+        torch.cuda.synchronize()
+        g_acc, g_nxt = acc.cpu().numpy(), nxt.cpu().numpy()
+        glog = logits.cpu().numpy().reshape(B, k + 1, CFG.vocab)
+        new_pending = []
+        for b in range(B):
+            r = verify_request(CFG, W, kvs[b], pending[b], drafts[b])
+            s = compare_request(r["logits"], glog[b], drafts[b], r["accept"], r["next"],
+                                int(g_acc[b]), int(g_nxt[b]), report, f"step {step} req {b}")
+            stats.append(s)
+            # both sides continue from the ORACLE's decision
+            commit_request(kvs[b], r)
+            hist[b] += [pending[b]] + drafts[b][: r["accept"]]
+            new_pending.append(r["next"])
+            # the GPU committed its own accept length: compare cached KV up to the shorter one
+            n_cmp = int(ctx_before[b]) + 1 + min(int(g_acc[b]), r["accept"])
+            for l in range(CFG.n_layers):
+                g = pool.gather_kv(b, n_cmp, l).double().cpu().numpy()
+                K, V = kvs[b].get(l)
+                np.testing.assert_allclose(g[0], K[:, :n_cmp], atol=2e-2, rtol=2e-2)
+                np.testing.assert_allclose(g[1], V[:, :n_cmp], atol=2e-2, rtol=2e-2)
+        # keep the GPU's ctx in step with the oracle (a near-tie could make them differ)
+        if not np.array_equal(ctx.cpu().numpy(), [kv.length for kv in kvs]):
+            report.append(f"step {step}: GPU committed a different length; resynchronising")
+            return stats
+        pending = new_pending
+    return stats
+
+
+@pytest.mark.parametrize("mode", ["suffix", "greedy", "mixed"])
+def test_verify_steps_match_oracle(tiny, mode):
+    report = []
+    stats = _run_steps(tiny, 3 if mode != "greedy" else 2, mode, seed={"suffix": 1, "greedy": 2, "mixed": 3}[mode],
+                       report=report)
+    print(f"\n[{mode}] max logit err {max(s['err'] for s in stats):.3e}; reported: {len(report)}")
+    for line in report:
+        print("  ", line)
+    assert max(s["err"] for s in stats) < 5e-2
+
+
+def test_full_accept_with_decisive_lm_head():
+    """LM head std x10 (top-2 gaps far above the rounding error): drafts equal
+    to the oracle's greedy continuation must be accepted exactly."""
+    war = _war()
+    w_cpu = synth.model_weights(CFG, seed=3, norm_std=0.1, lm_std=0.2)
+    W = Weights(CFG, w_cpu)
+    model = war.Model(CFG, {k: v.to(DEV) for k, v in w_cpu.items()}, max_rows=64)
+    tiny = {"war": war, "W": W, "model": model}
+    _, ctxs = _tiny_workload(seed=4, B=4, ctx_len=200)
+    pool, seq, ctx, kvs, onext, ologits, gnext, glogits = _prefill_both(tiny, ctxs)
+    assert (gnext == onext).all()
+    k = 5
+    drafts = [greedy_decode(CFG, W, copy.deepcopy(kvs[b]), int(onext[b]), k + 1) for b in range(4)]
+    dt = torch.tensor([d[:k] for d in drafts], dtype=torch.int32, device=DEV)
+    acc = torch.zeros(4, dtype=torch.int32, device=DEV)
+    nxt = torch.zeros(4, dtype=torch.int32, device=DEV)
+    war.verify_step(model, pool, seq, ctx, torch.tensor(onext, dtype=torch.int32, device=DEV), dt,
+                    None, k, acc, nxt)
+    war.kv_commit(pool, seq, ctx, acc)
+    assert acc.cpu().tolist() == [k] * 4
+    assert nxt.cpu().tolist() == [d[k] for d in drafts]
+    assert ctx.cpu().tolist() == [len(c) + k + 1 for c in ctxs]
