@@ -27,6 +27,17 @@ war_status war_debug_mfma16(const void* A, const void* B, float* C, void* stream
  * until the next call on the model. */
 war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes);
 
+/* Per-kernel timing.  war_profile(m, 1) clears the record and starts timing
+ * every kernel launch of later verify/prefill calls on this model.  Each
+ * launch is bracketed by a pair of HIP events on the launch stream.
+ * war_profile(m, 0) stops.
+ * war_profile_read synchronises the device and writes one line per kernel,
+ * "name calls total_ms\n", into out (HOST, out_len bytes).  It then clears
+ * the record.  The event pairs add a few microseconds per launch, so time
+ * whole steps without profiling. */
+war_status war_profile(war_model* m, int32_t enable);
+war_status war_profile_read(war_model* m, char* out, int32_t out_len);
+
 #ifdef __cplusplus
 }
 #endif

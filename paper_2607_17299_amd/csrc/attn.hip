@@ -43,6 +43,8 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
   const int total = a.meta.n_items[0] * a.n_kv_heads;
   const int P = a.kv.page_size;
+  // key row of this lane in S^T tile t (within a 32-key block); tile 1 adds 4
+  const int kk0 = (ln >> 2) * 8 + (ln & 3);
 
   for (int it = blockIdx.x; it < total; it += gridDim.x) {
     const int item = it / a.n_kv_heads, kvh = it % a.n_kv_heads;
@@ -89,80 +91,98 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
     const int wk0 = kbeg + w * CW, wk1 = min(kend, wk0 + CW);
     const int32_t* trow = a.table + (int64_t)seq * a.max_pages;
     const bf16_t* kvl = a.kv.kv;
-    // key row of this lane in S^T tile t (within a 32-key block)
-    const int kk0 = (ln >> 2) * 8 + (ln & 3);  // tile 0; tile 1 adds 4
 
-    for (int kb = wk0; kb < wk1; kb += 32) {
+    // K fragments (A operand, lane (m = ln, g = lg)) and V^T fragments (A operand of
+    // the second product, lane (m = dim, g = lg) -> keys lg*8..+7) of a 32-key block
+    uint4 kf[2][KSUB], vf[NDT];
+    auto load_block = [&](int kb) {
       const int pg0 = trow[kb / P];
       const int pg1 = (kb + 16 < S) ? trow[kb / P + 1] : pg0;
-      // K fragments: A operand, lane (m = ln, g = lg)
-      bf16x8 kf[2][KSUB];
 #pragma unroll
       for (int t = 0; t < 2; ++t) {
         const int kk = kk0 + 4 * t;
         const int pg = kk < 16 ? pg0 : pg1;
         const bf16_t* kp = kvl + a.kv.page_elems(a.layer, pg, kvh, 0) + (kk & 15) * HD + lg * DPL;
 #pragma unroll
-        for (int j = 0; j < KSUB; ++j) kf[t][j] = as_bf16x8(*reinterpret_cast<const uint4*>(kp + j * 8));
+        for (int j = 0; j < KSUB; ++j) kf[t][j] = *reinterpret_cast<const uint4*>(kp + j * 8);
       }
-      // V^T fragments: A operand of the second product, lane (m = dim, g = lg) -> keys lg*8..+7
-      bf16x8 vf[NDT];
-      {
-        const int pg = lg < 2 ? pg0 : pg1;
-        const bf16_t* vp = kvl + a.kv.page_elems(a.layer, pg, kvh, 1) + (lg & 1) * 8;
-        if (kb + 32 <= S) {
+      const int pg = lg < 2 ? pg0 : pg1;
+      const bf16_t* vp = kvl + a.kv.page_elems(a.layer, pg, kvh, 1) + (lg & 1) * 8;
 #pragma unroll
-          for (int dt = 0; dt < NDT; ++dt)
-            vf[dt] = as_bf16x8(*reinterpret_cast<const uint4*>(vp + (dt * 16 + ln) * P));
-        } else {  // the sequence ends inside this block
-          const int nvalid = min(max(S - (kb + lg * 8), 0), 8);
+      for (int dt = 0; dt < NDT; ++dt) vf[dt] = *reinterpret_cast<const uint4*>(vp + (dt * 16 + ln) * P);
+      if (kb + 32 > S) {  // the sequence ends inside this block
+        const int nvalid = min(max(S - (kb + lg * 8), 0), 8);
 #pragma unroll
-          for (int dt = 0; dt < NDT; ++dt)
-            vf[dt] = as_bf16x8(keep_first(*reinterpret_cast<const uint4*>(vp + (dt * 16 + ln) * P), nvalid));
-        }
+        for (int dt = 0; dt < NDT; ++dt) vf[dt] = keep_first(vf[dt], nvalid);
       }
+    };
+
+    if (wk0 < wk1) load_block(wk0);
+    for (int kb = wk0; kb < wk1; kb += 32) {
+      bf16x8 kc[2][KSUB], vc[NDT];
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int j = 0; j < KSUB; ++j) kc[t][j] = as_bf16x8(kf[t][j]);
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) vc[dt] = as_bf16x8(vf[dt]);
+      if (kb + 32 < wk1) load_block(kb + 32);  // in flight while this block computes
+
+      // keys of this block above the smallest row position need the causal mask
+      const bool tail = kb + 31 > pos0 + t0;
 #pragma unroll
       for (int rt = 0; rt < NR; ++rt) {
         f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < KSUB; ++j) {
-          s0 = mfma16(kf[0][j], qf[rt][j], s0);
-          s1 = mfma16(kf[1][j], qf[rt][j], s1);
+          s0 = mfma16(kc[0][j], qf[rt][j], s0);
+          s1 = mfma16(kc[1][j], qf[rt][j], s1);
         }
         // lane holds S^T[key kb + lg*8 + 4t + i][row rt*16 + ln]
-        float sv[8];
+        float sv[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+        if (tail) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int k0 = kb + lg * 8 + i;
-          sv[i] = k0 <= rpos[rt] ? s0[i] * a.scale_log2 : -INFINITY;
-          sv[4 + i] = k0 + 4 <= rpos[rt] ? s1[i] * a.scale_log2 : -INFINITY;
+          for (int e = 0; e < 8; ++e)
+            if (kb + lg * 8 + e > rpos[rt]) sv[e] = -INFINITY;
         }
-        float mx = sv[0];
+        float lm = sv[0];
 #pragma unroll
-        for (int e = 1; e < 8; ++e) mx = fmaxf(mx, sv[e]);
-        mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-        mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-        const float m_new = fmaxf(m_run[rt], mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2f(m_run[rt] - m_use);
-        float pe[8], sum = 0.f;
+        for (int e = 1; e < 8; ++e) lm = fmaxf(lm, sv[e]);
+        lm *= a.scale_log2;
+        // Lazy rescaling: the running max only moves when a score exceeds it by
+        // more than 2^8 (weights stay below 256, exact in fp32); the decision is
+        // taken for the whole wave so the 4 lanes of a row always agree.
+        if (__any(lm > m_run[rt] + 8.f)) {
+          float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
+          mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+          const float m_new = fmaxf(m_run[rt], mx);
+          if (m_new > m_run[rt]) {
+            const float alpha = exp2f(m_run[rt] - m_new);
+            l_run[rt] *= alpha;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) {
-          pe[e] = round_bf(exp2f(sv[e] - m_use));
-          sum += pe[e];
+            for (int dt = 0; dt < NDT; ++dt) o_acc[dt][rt] *= alpha;
+            m_run[rt] = m_new;
+          }
         }
-        l_run[rt] = l_run[rt] * alpha + sum;
-        m_run[rt] = m_new;
-        uint4 pp;
-        pp.x = pack2(pe[0], pe[1]);
-        pp.y = pack2(pe[2], pe[3]);
-        pp.z = pack2(pe[4], pe[5]);
-        pp.w = pack2(pe[6], pe[7]);
-        const bf16x8 pf = as_bf16x8(pp);
+        const float m_use = m_run[rt] == -INFINITY ? 0.f : m_run[rt];
+        // P = hi + lo, both bf16: the product keeps ~16 bits of each weight
+        float sum = 0.f;
+        uint32_t hi[4], lo[4];
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const float p0 = exp2f(fmaf(sv[e], a.scale_log2, -m_use));
+          const float p1 = exp2f(fmaf(sv[e + 1], a.scale_log2, -m_use));
+          sum += p0 + p1;
+          hi[e / 2] = pack2(p0, p1);
+          lo[e / 2] = pack2(p0 - lo_f(hi[e / 2]), p1 - hi_f(hi[e / 2]));
+        }
+        l_run[rt] += sum;
+        const bf16x8 ph = as_bf16x8(make_uint4(hi[0], hi[1], hi[2], hi[3]));
+        const bf16x8 pl = as_bf16x8(make_uint4(lo[0], lo[1], lo[2], lo[3]));
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-          o_acc[dt][rt] *= alpha;
-          o_acc[dt][rt] = mfma16(vf[dt], pf, o_acc[dt][rt]);
+          o_acc[dt][rt] = mfma16(vc[dt], ph, o_acc[dt][rt]);
+          o_acc[dt][rt] = mfma16(vc[dt], pl, o_acc[dt][rt]);
         }
       }
     }
@@ -202,12 +222,14 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
       }
       __syncthreads();
     }
+    // partial of the live rows only: [item][kvh][row][dim] with row stride HD
     const int64_t pbase = ((int64_t)item * a.n_kv_heads + kvh) * RB;
-    for (int e = tid; e < RB * HD; e += 256) {
-      const int r = e / HD, d = e % HD;
-      a.po[(pbase + r) * HD + d] = s_o[r * OST + d];
+    for (int e = tid; e < nrows * (HD / 4); e += 256) {
+      const int r = e / (HD / 4), d4 = (e % (HD / 4)) * 4;
+      const float* src = &s_o[r * OST + d4];
+      *reinterpret_cast<float4*>(&a.po[(pbase + r) * HD + d4]) = make_float4(src[0], src[1], src[2], src[3]);
     }
-    if (tid < RB) {
+    if (tid < nrows) {
       const int r = tid;
       const float mm = fmaxf(fmaxf(s_m[0][r], s_m[1][r]), fmaxf(s_m[2][r], s_m[3][r]));
       const float mu = mm == -INFINITY ? 0.f : mm;
@@ -221,30 +243,62 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
 }
 
 // Merge a (request, row block)'s chunk partials in item order; o = sum / l -> bf16.
+// Workgroup = (segment, kv-head, 16-row slice): the per-item weights
+// exp2(m_i - m) / l of its rows go to LDS, then every thread accumulates float4
+// runs of the output with all of its loads independent.
+constexpr int kCombMaxItems = 512;
 template <int RB, int HD>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
-  const int seg = blockIdx.x, kvh = blockIdx.y;
+  __shared__ float s_w[16][kCombMaxItems];
+  __shared__ float s_mx[16];
+  const int seg = blockIdx.x, kvh = blockIdx.y, r0 = blockIdx.z * 16;
   const int b = a.meta.seg_req[seg];
   const int t0 = a.meta.seg_rb[seg] * a.TB;
   const int nt = min(a.TB, a.meta.req_ntok[b] - t0);
-  if (nt <= 0) return;
   const int nrows = nt * a.G;
-  const int ib = a.meta.seg_begin[seg], ni = a.meta.seg_count[seg];
+  if (nt <= 0 || r0 >= nrows) return;
+  const int rows = min(16, nrows - r0);
+  const int ib = a.meta.seg_begin[seg], ni = min(a.meta.seg_count[seg], kCombMaxItems);
   const int row0 = a.meta.req_row0[b];
-  for (int e = threadIdx.x; e < nrows * HD; e += blockDim.x) {
-    const int r = e / HD, d = e % HD;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  // one wave per row: max, then the normalised weights
+  for (int r = w; r < rows; r += 4) {
     float mm = -INFINITY;
-    for (int i = 0; i < ni; ++i)
-      mm = fmaxf(mm, a.pm[((int64_t)(ib + i) * a.n_kv_heads + kvh) * RB + r]);
-    float l = 0.f, o = 0.f;
-    for (int i = 0; i < ni; ++i) {
-      const int64_t pb = ((int64_t)(ib + i) * a.n_kv_heads + kvh) * RB + r;
+    for (int i = lane; i < ni; i += 64)
+      mm = fmaxf(mm, a.pm[((int64_t)(ib + i) * a.n_kv_heads + kvh) * RB + r0 + r]);
+    mm = wave_max(mm);
+    float l = 0.f;
+    for (int i = lane; i < ni; i += 64) {
+      const int64_t pb = ((int64_t)(ib + i) * a.n_kv_heads + kvh) * RB + r0 + r;
       const float f = exp2f(a.pm[pb] - mm);
+      s_w[r][i] = f;
       l += a.pl[pb] * f;
-      o += a.po[pb * HD + d] * f;
     }
-    const int ti = t0 + r / a.G, h = kvh * a.G + r % a.G;
-    a.o[(int64_t)(row0 + ti) * a.q_stride + h * HD + d] = f2bf(o / l);
+    l = wave_sum(l);
+    if (lane == 0) s_mx[r] = 1.f / l;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < rows * (HD / 4); e += blockDim.x) {
+    const int r = e / (HD / 4), d4 = (e % (HD / 4)) * 4;
+    float4 acc = {0.f, 0.f, 0.f, 0.f};
+    const float* base = a.po + ((int64_t)ib * a.n_kv_heads + kvh) * RB * HD + (int64_t)(r0 + r) * HD + d4;
+    const int64_t stride = (int64_t)a.n_kv_heads * RB * HD;
+    for (int i = 0; i < ni; ++i) {
+      const float4 v = *reinterpret_cast<const float4*>(base + i * stride);
+      const float f = s_w[r][i];
+      acc.x += v.x * f;
+      acc.y += v.y * f;
+      acc.z += v.z * f;
+      acc.w += v.w * f;
+    }
+    const float inv = s_mx[r];
+    const int rr = r0 + r;
+    const int ti = t0 + rr / a.G, h = kvh * a.G + rr % a.G;
+    bf16_t* dst = a.o + (int64_t)(row0 + ti) * a.q_stride + h * HD + d4;
+    uint2 o;
+    o.x = pack2(acc.x * inv, acc.y * inv);
+    o.y = pack2(acc.z * inv, acc.w * inv);
+    *reinterpret_cast<uint2*>(dst) = o;
   }
 }
 
@@ -258,7 +312,7 @@ void launch_attn_nr(const AttnArgs& a, int head_dim, int grid, hipStream_t st) {
 
 template <int RB>
 void launch_comb(const AttnArgs& a, int head_dim, int n_segs, hipStream_t st) {
-  dim3 grid(n_segs, a.n_kv_heads);
+  dim3 grid(n_segs, a.n_kv_heads, RB / 16);
   if (head_dim == 128)
     k_attn_combine<RB, 128><<<grid, 256, 0, st>>>(a);
   else

@@ -13,20 +13,21 @@ typedef uint16_t bf16_t;  // raw bfloat16 bits in memory
 // ------------------------------------------------------------------ bf16 bits
 WAR_DEV float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
 
-// float -> bfloat16 bits, round to nearest even; NaN stays NaN (quietened).
-WAR_DEV bf16_t f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16_t)(u >> 16);
-}
+// float -> bfloat16 bits, round to nearest even (gfx950 v_cvt_pk_bf16_f32).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+WAR_DEV bf16_t f2bf(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 // round a float to the nearest bfloat16 value, kept as float
 WAR_DEV float round_bf(float f) { return bf2f(f2bf(f)); }
 
 WAR_DEV uint32_t pack2(float a, float b) {
-  return (uint32_t)f2bf(a) | ((uint32_t)f2bf(b) << 16);
+  const bf16x2_t v = {(__bf16)a, (__bf16)b};
+  return __builtin_bit_cast(uint32_t, v);
 }
+
+// the two floats held by a packed bf16 pair
+WAR_DEV float lo_f(uint32_t v) { return __uint_as_float(v << 16); }
+WAR_DEV float hi_f(uint32_t v) { return __uint_as_float(v & 0xffff0000u); }
 
 WAR_DEV bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 

@@ -59,23 +59,38 @@ __global__ void __launch_bounds__(256) k_embed_norm(const int32_t* tok, const bf
   norm_row(hr, d, g, eps, u + (int64_t)r * d, ss, red);
 }
 
-// h += sum_s P[s]; u = norm(h) * g
-__global__ void __launch_bounds__(256) k_residual_norm(int rows, int splits, const float* P, int d,
-                                                       const bf16_t* g, float eps, float* h,
-                                                       bf16_t* u) {
+// Sum of the split-K partials of one float4 run: all loads issued before use.
+__device__ __forceinline__ float4 sum_splits(const float* P, int64_t sstride, int splits, float4 x) {
+  int s = 0;
+  for (; s + 4 <= splits; s += 4) {
+    const float4 a = *reinterpret_cast<const float4*>(P + (s + 0) * sstride);
+    const float4 b = *reinterpret_cast<const float4*>(P + (s + 1) * sstride);
+    const float4 c = *reinterpret_cast<const float4*>(P + (s + 2) * sstride);
+    const float4 d = *reinterpret_cast<const float4*>(P + (s + 3) * sstride);
+    x.x += a.x; x.y += a.y; x.z += a.z; x.w += a.w;
+    x.x += b.x; x.y += b.y; x.z += b.z; x.w += b.w;
+    x.x += c.x; x.y += c.y; x.z += c.z; x.w += c.w;
+    x.x += d.x; x.y += d.y; x.z += d.z; x.w += d.w;
+  }
+  for (; s < splits; ++s) {
+    const float4 a = *reinterpret_cast<const float4*>(P + s * sstride);
+    x.x += a.x; x.y += a.y; x.z += a.z; x.w += a.w;
+  }
+  return x;
+}
+
+// h += sum_s P[s]; u = norm(h) * g   (one 1024-thread workgroup per row)
+__global__ void __launch_bounds__(1024) k_residual_norm(int rows, int splits, const float* P, int d,
+                                                        const bf16_t* g, float eps, float* h,
+                                                        bf16_t* u) {
   __shared__ float red[16];
   const int r = blockIdx.x;
   float* hr = h + (int64_t)r * d;
+  const int64_t sstride = (int64_t)rows * d;
   float ss = 0.f;
   for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
     float4 x = *reinterpret_cast<const float4*>(hr + c);
-    for (int s = 0; s < splits; ++s) {
-      const float4 p = *reinterpret_cast<const float4*>(P + ((int64_t)s * rows + r) * d + c);
-      x.x += p.x;
-      x.y += p.y;
-      x.z += p.z;
-      x.w += p.w;
-    }
+    x = sum_splits(P + (int64_t)r * d + c, sstride, splits, x);
     ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
     *reinterpret_cast<float4*>(hr + c) = x;
   }
@@ -95,6 +110,8 @@ __global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const fl
   const int nq_pairs = md.nq * half, nk_pairs = md.nkv * half;
   const int n_pairs = md.qkv / 2;
   const bool act = meta.active[r] != 0;
+  const int p = blockIdx.y * blockDim.x + threadIdx.x;
+  if (p >= n_pairs) return;
   int page = 0, slot = 0;
   if (act) {
     const int pos = meta.pos[r];
@@ -104,7 +121,7 @@ __global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const fl
   }
   const float* pr = P + (int64_t)r * md.qkv;
   const int64_t pstride = (int64_t)rows * md.qkv;
-  for (int p = threadIdx.x; p < n_pairs; p += blockDim.x) {
+  {
     int region, head, j;
     if (p < nq_pairs) {
       region = 0;
@@ -122,6 +139,7 @@ __global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const fl
     const int col = (region == 0 ? 0 : region == 1 ? md.nq * md.hd : (md.nq + md.nkv) * md.hd) +
                     head * md.hd + j;
     float x1 = 0.f, x2 = 0.f;
+#pragma unroll 8
     for (int s = 0; s < splits; ++s) {
       x1 += pr[s * pstride + col];
       x2 += pr[s * pstride + col + half];
@@ -154,22 +172,19 @@ __global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const fl
 __global__ void __launch_bounds__(256) k_swiglu(int rows, int splits, const float* P, int F,
                                                 bf16_t* y) {
   const int r = blockIdx.x;
+  const int c = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
+  if (c >= F) return;
   const int64_t N = 2 * (int64_t)F;
-  for (int c = threadIdx.x * 4; c < F; c += blockDim.x * 4) {
-    float4 gt = {0.f, 0.f, 0.f, 0.f}, up = {0.f, 0.f, 0.f, 0.f};
-    for (int s = 0; s < splits; ++s) {
-      const float* ps = P + ((int64_t)s * rows + r) * N;
-      const float4 a = *reinterpret_cast<const float4*>(ps + c);
-      const float4 b = *reinterpret_cast<const float4*>(ps + F + c);
-      gt.x += a.x; gt.y += a.y; gt.z += a.z; gt.w += a.w;
-      up.x += b.x; up.y += b.y; up.z += b.z; up.w += b.w;
-    }
-    auto sw = [](float a, float b) { return a / (1.f + expf(-a)) * b; };
-    uint2 o;
-    o.x = pack2(sw(gt.x, up.x), sw(gt.y, up.y));
-    o.y = pack2(sw(gt.z, up.z), sw(gt.w, up.w));
-    *reinterpret_cast<uint2*>(y + (int64_t)r * F + c) = o;
-  }
+  const int64_t sstride = (int64_t)rows * N;
+  const float* ps = P + (int64_t)r * N + c;
+  const float4 z = {0.f, 0.f, 0.f, 0.f};
+  const float4 gt = sum_splits(ps, sstride, splits, z);
+  const float4 up = sum_splits(ps + F, sstride, splits, z);
+  auto sw = [](float a, float b) { return a / (1.f + expf(-a)) * b; };
+  uint2 o;
+  o.x = pack2(sw(gt.x, up.x), sw(gt.y, up.y));
+  o.y = pack2(sw(gt.z, up.z), sw(gt.w, up.w));
+  *reinterpret_cast<uint2*>(y + (int64_t)r * F + c) = o;
 }
 
 // Per request: greedy token of each active row (best over the LM head's column
@@ -243,17 +258,19 @@ void launch_embed_norm(int rows, const int32_t* tok, const bf16_t* E, const bf16
 }
 void launch_residual_norm(int rows, int splits, const float* P, int d, const bf16_t* g, float eps,
                           float* h, bf16_t* u, hipStream_t st) {
-  k_residual_norm<<<rows, 256, 0, st>>>(rows, splits, P, d, g, eps, h, u);
+  k_residual_norm<<<rows, 1024, 0, st>>>(rows, splits, P, d, g, eps, h, u);
 }
 void launch_qkv_rope(int rows, int splits, const float* P, const ModelDims& md,
                      const float* cos_t, const float* sin_t, const StepMeta& meta,
                      const int32_t* row_req, const int32_t* table, int max_pages, const KvGeom& kv,
                      int layer, bf16_t* q, hipStream_t st) {
-  k_qkv_rope<<<rows, 256, 0, st>>>(rows, splits, P, md, cos_t, sin_t, meta, row_req, table,
+  dim3 grid(rows, cdiv_i(md.qkv / 2, 256));
+  k_qkv_rope<<<grid, 256, 0, st>>>(rows, splits, P, md, cos_t, sin_t, meta, row_req, table,
                                    max_pages, kv, layer, q);
 }
 void launch_swiglu(int rows, int splits, const float* P, int F, bf16_t* y, hipStream_t st) {
-  k_swiglu<<<rows, 256, 0, st>>>(rows, splits, P, F, y);
+  dim3 grid(rows, cdiv_i(F / 4, 256));
+  k_swiglu<<<grid, 256, 0, st>>>(rows, splits, P, F, y);
 }
 void launch_argmax_accept(int n_req, const int32_t* ntok, int row_stride, int n_blocks,
                           const float* amax_v, const int32_t* amax_i, const int32_t* draft_tokens,

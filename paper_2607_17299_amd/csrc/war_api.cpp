@@ -66,7 +66,25 @@ struct LayerW {
 };
 
 constexpr int kMaxBatch = 1024;
+
+// Opt-in per-kernel timing: HIP events recorded on the launch stream around
+// every kernel launch, summed per kernel name when read back.
+struct Profiler {
+  bool on = false;
+  std::vector<hipEvent_t> pool;
+  size_t used = 0;
+  std::vector<std::pair<std::string, std::pair<size_t, size_t>>> marks;
+  hipEvent_t next() {
+    if (used == pool.size()) {
+      hipEvent_t e;
+      if (hipEventCreate(&e) != hipSuccess) return nullptr;
+      pool.push_back(e);
+    }
+    return pool[used++];
+  }
+};
 constexpr int kPrefillChunk = 1024;  // keys per attention item when prefilling
+constexpr int kMaxItemsPerSeq = 512;  // attention chunks one combine merges
 constexpr int64_t kPartialCap = int64_t(64) << 20;  // fp32 split-K partial elements
 
 }  // namespace
@@ -90,6 +108,7 @@ struct war_model {
   DevBuf stage_dev;              // device copy of per-prefill host arrays
   int32_t* pinned = nullptr;     // pinned host staging
   size_t pinned_ints = 0;
+  Profiler prof;
 
   StepMeta meta() const {
     StepMeta m;
@@ -169,12 +188,39 @@ struct Split {
   int s, kper;
 };
 
+// Records an event pair around the launches in its scope when profiling is on.
+struct Timed {
+  Profiler& p;
+  hipStream_t st;
+  size_t i0 = 0;
+  const char* name;
+  bool act;
+  Timed(Profiler& pr, hipStream_t s, const char* n) : p(pr), st(s), name(n), act(pr.on) {
+    if (act) {
+      i0 = p.used;
+      hipEvent_t e = p.next();
+      if (e) (void)hipEventRecord(e, st);
+      else act = false;
+    }
+  }
+  ~Timed() {
+    if (act) {
+      const size_t i1 = p.used;
+      hipEvent_t e = p.next();
+      if (e) {
+        (void)hipEventRecord(e, st);
+        p.marks.push_back({name, {i0, i1}});
+      }
+    }
+  }
+};
+
 Split pick_split(int M, int N, int K, int64_t cap_elems) {
   const int mt = gemm_mt(M);
   const int mblocks = cdiv_i(M, mt * 16);
   const int base = (N / 128) * mblocks;
   int s = std::max(1, (int)std::lround(1024.0 / base));
-  s = std::min(s, std::max(1, K / 256));
+  s = std::min(s, std::max(1, K / 512));
   while (s > 1 && (int64_t)s * M * N > cap_elems) --s;
   int kper = cdiv_i(cdiv_i(K, s), 64) * 64;
   s = cdiv_i(K, kper);
@@ -220,26 +266,63 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
   bf16_t* q = m->q.as<bf16_t>();
   bf16_t* o = m->o.as<bf16_t>();
   float* P = m->P.as<float>();
-  launch_rope_table(R, meta.pos, m->inv_freq.as<double>(), md.hd / 2, m->cos_t.as<float>(),
-                    m->sin_t.as<float>(), st);
-  launch_embed_norm(R, meta.tok, m->embed, m->layers[0].attn_norm, md.d, md.eps, h, u, st);
+  Profiler& pf = m->prof;
+  {
+    Timed t(pf, st, "rope_table");
+    launch_rope_table(R, meta.pos, m->inv_freq.as<double>(), md.hd / 2, m->cos_t.as<float>(),
+                      m->sin_t.as<float>(), st);
+  }
+  {
+    Timed t(pf, st, "embed_norm");
+    launch_embed_norm(R, meta.tok, m->embed, m->layers[0].attn_norm, md.d, md.eps, h, u, st);
+  }
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW& L = m->layers[l];
     int s = 1;
-    gemm(m, u, md.d, nullptr, L.w_qkv, nullptr, 0, R, md.qkv, md.d, &s, st);
-    launch_qkv_rope(R, s, P, md, m->cos_t.as<float>(), m->sin_t.as<float>(), meta, meta.row_req,
-                    p->dev.table, p->dev.max_pages, p->geom, l, q, st);
+    {
+      Timed t(pf, st, "gemm_qkv");
+      gemm(m, u, md.d, nullptr, L.w_qkv, nullptr, 0, R, md.qkv, md.d, &s, st);
+    }
+    {
+      Timed t(pf, st, "qkv_rope_kvwrite");
+      launch_qkv_rope(R, s, P, md, m->cos_t.as<float>(), m->sin_t.as<float>(), meta, meta.row_req,
+                      p->dev.table, p->dev.max_pages, p->geom, l, q, st);
+    }
     AttnArgs a = attn_base;
     a.layer = l;
-    launch_attn(a, RB, md.hd, attn_grid, st);
-    launch_attn_combine(a, RB, md.hd, n_segs, st);
-    gemm(m, o, md.nq * md.hd, nullptr, L.w_o, nullptr, 0, R, md.d, md.nq * md.hd, &s, st);
-    launch_residual_norm(R, s, P, md.d, L.ffn_norm, md.eps, h, u, st);
-    gemm(m, u, md.d, nullptr, L.w_gate, L.w_up, md.F, R, 2 * md.F, md.d, &s, st);
-    launch_swiglu(R, s, P, md.F, u, st);
-    gemm(m, u, md.F, nullptr, L.w_down, nullptr, 0, R, md.d, md.F, &s, st);
+    {
+      Timed t(pf, st, "attention");
+      launch_attn(a, RB, md.hd, attn_grid, st);
+    }
+    {
+      Timed t(pf, st, "attn_combine");
+      launch_attn_combine(a, RB, md.hd, n_segs, st);
+    }
+    {
+      Timed t(pf, st, "gemm_o");
+      gemm(m, o, md.nq * md.hd, nullptr, L.w_o, nullptr, 0, R, md.d, md.nq * md.hd, &s, st);
+    }
+    {
+      Timed t(pf, st, "residual_norm");
+      launch_residual_norm(R, s, P, md.d, L.ffn_norm, md.eps, h, u, st);
+    }
+    {
+      Timed t(pf, st, "gemm_gate_up");
+      gemm(m, u, md.d, nullptr, L.w_gate, L.w_up, md.F, R, 2 * md.F, md.d, &s, st);
+    }
+    {
+      Timed t(pf, st, "swiglu");
+      launch_swiglu(R, s, P, md.F, u, st);
+    }
+    {
+      Timed t(pf, st, "gemm_down");
+      gemm(m, u, md.F, nullptr, L.w_down, nullptr, 0, R, md.d, md.F, &s, st);
+    }
     const bf16_t* gnext = l + 1 < m->cfg.n_layers ? m->layers[l + 1].attn_norm : m->final_norm;
-    launch_residual_norm(R, s, P, md.d, gnext, md.eps, h, u, st);
+    {
+      Timed t(pf, st, "residual_norm");
+      launch_residual_norm(R, s, P, md.d, gnext, md.eps, h, u, st);
+    }
   }
   HIPCHK(hipGetLastError());
   return WAR_OK;
@@ -392,6 +475,7 @@ void war_model_destroy(war_model* m) {
                     &m->items, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
     b->release();
   if (m->pinned) (void)hipHostFree(m->pinned);
+  for (hipEvent_t e : m->prof.pool) (void)hipEventDestroy(e);
   delete m;
 }
 
@@ -603,6 +687,7 @@ war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_
   const int RB = attn_rows_per_block(G, kp1);
   int chunk = 256;
   while (chunk < 2048 && chunk * 2 <= G * kp1 * 32) chunk *= 2;
+  while (cdiv_i(p->dev.max_pages * P, chunk) > kMaxItemsPerSeq) chunk *= 2;
   const int64_t max_items = (int64_t)B * cdiv_i(p->dev.max_pages * P, chunk);
   war_status s = ensure_items(m, max_items, RB);
   if (s != WAR_OK) return s;
@@ -617,17 +702,26 @@ war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_
   va.last_tokens = last_tokens;
   va.draft_tokens = draft_tokens;
   va.draft_lens = draft_lens;
-  launch_verify_setup(p->dev, va, m->meta(), st);
+  {
+    Timed t(m->prof, st, "verify_setup");
+    launch_verify_setup(p->dev, va, m->meta(), st);
+  }
 
   AttnArgs a = attn_args(m, p, kp1, chunk);
   const int grid = (int)std::min<int64_t>(max_items * m->md.nkv, RB == 48 ? 1024 : 2048);
   s = run_layers(m, p, R, a, RB, grid, B, st);
   if (s != WAR_OK) return s;
   int sdummy;
-  gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, nullptr, 0, R, m->md.V, m->md.d, &sdummy, st,
-       true, logits);
-  launch_argmax_accept(B, m->meta().req_ntok, kp1, m->md.V / 128, m->amax_v.as<float>(),
-                       m->amax_i.as<int32_t>(), draft_tokens, k_max, accept_lens, next_tokens, st);
+  {
+    Timed t(m->prof, st, "gemm_lm_head_argmax");
+    gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, nullptr, 0, R, m->md.V, m->md.d, &sdummy,
+         st, true, logits);
+  }
+  {
+    Timed t(m->prof, st, "argmax_accept");
+    launch_argmax_accept(B, m->meta().req_ntok, kp1, m->md.V / 128, m->amax_v.as<float>(),
+                         m->amax_i.as<int32_t>(), draft_tokens, k_max, accept_lens, next_tokens, st);
+  }
   HIPCHK(hipGetLastError());
   p->free_lb -= need;
   p->pending = true;
@@ -700,7 +794,8 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
   // forward over chunks of at most max_rows packed rows
   const int RB = 48;
   const int TB = RB / G;
-  const int chunk = kPrefillChunk;
+  int chunk = kPrefillChunk;
+  while (cdiv_i(p->dev.max_pages * P, chunk) > kMaxItemsPerSeq) chunk *= 2;
   std::vector<int64_t> cu(n + 1, 0);
   for (int i = 0; i < n; ++i) cu[i + 1] = cu[i] + n_new_host[i];
   const int R_cap = m->max_rows;
@@ -795,6 +890,43 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
   HIPCHK(hipGetLastError());
   HIPCHK(hipStreamSynchronize(st));
   return WAR_OK;
+}
+
+war_status war_profile(war_model* m, int32_t enable) {
+  CHECK(m, "null model");
+  m->prof.on = enable != 0;
+  m->prof.used = 0;
+  m->prof.marks.clear();
+  return WAR_OK;
+}
+
+war_status war_profile_read(war_model* m, char* out, int32_t out_len) {
+  CHECK(m && out && out_len > 0, "null argument");
+  HIPCHK(hipDeviceSynchronize());
+  std::vector<std::string> names;
+  std::vector<double> ms;
+  std::vector<int> calls;
+  for (auto& mk : m->prof.marks) {
+    float t = 0.f;
+    HIPCHK(hipEventElapsedTime(&t, m->prof.pool[mk.second.first], m->prof.pool[mk.second.second]));
+    size_t i = 0;
+    while (i < names.size() && names[i] != mk.first) ++i;
+    if (i == names.size()) {
+      names.push_back(mk.first);
+      ms.push_back(0.0);
+      calls.push_back(0);
+    }
+    ms[i] += t;
+    calls[i] += 1;
+  }
+  std::string text;
+  for (size_t i = 0; i < names.size(); ++i)
+    text += names[i] + " " + std::to_string(calls[i]) + " " + std::to_string(ms[i]) + "\n";
+  std::strncpy(out, text.c_str(), (size_t)out_len - 1);
+  out[out_len - 1] = 0;
+  m->prof.used = 0;
+  m->prof.marks.clear();
+  return (int64_t)text.size() < out_len ? WAR_OK : fail(WAR_ERR_INVALID_ARG, "profile text truncated");
 }
 
 war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes) {

@@ -1,0 +1,191 @@
+"""Synthetic rollout workloads for the verify step (test and benchmark harness).
+
+Builds, on one GPU, the state a verify step starts from: the decoder weights, a
+KV pool with each request's cached context, and the step's inputs (pending
+tokens and draft tokens from the host suffix drafter).  Everything is seeded.
+The cached context's keys and values are imported through ``war_kv_load`` from
+the seeded generator rather than recomputed by a prefill: the verify step's
+cost and arithmetic do not depend on how the cache was produced, and a prefill
+over hundreds of thousands of tokens would dominate every run.
+
+Workloads (the paper's setting; its SWE dataset and Qwen3-32B are not available):
+  low_load     8 requests x 32768 cached tokens built from recurring tool-call-
+               like motifs, k = 8 drafts from the suffix drafter over 64 prior
+               trajectories (System Design, "SuffixDecoding"; Evaluation).
+  high_load    64 requests, long-tailed lognormal contexts (median 8192,
+               sigma 0.8, clipped to [1024, 65536]), k = 0: plain batched decode.
+  high_load_k2 the same contexts, k = 2 drafts taken from a sibling rollout's
+               continuation with ~30% of the positions corrupted, so that
+               rejected slots are rolled back.
+  multi_turn   16 trajectories in 4 groups sharing an 8192-token prefix,
+               24576 cached tokens each; a 2048-token observation is appended
+               with war_prefill_append, then one k = 4 verify step.
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional
+
+import numpy as np
+import torch
+
+from . import synth, war
+from .drafter import SuffixDrafter
+
+LARGE_SEED = 1
+
+
+def cdiv(a: int, b: int) -> int:
+    return -(-a // b)
+
+
+def large_weights(cfg: synth.ModelConfig = synth.LARGE, device="cuda", seed: int = LARGE_SEED,
+                  lm_std: float = synth.WEIGHT_STD) -> Dict[str, torch.Tensor]:
+    return synth.model_weights(cfg, seed, device=device, lm_std=lm_std)
+
+
+@dataclasses.dataclass
+class Step:
+    """Inputs of one verify step, as host arrays."""
+    seq_ids: np.ndarray
+    ctx_lens: np.ndarray
+    last_tokens: np.ndarray
+    drafts: List[List[int]]
+    k_max: int
+
+    @property
+    def B(self) -> int:
+        return len(self.seq_ids)
+
+    def draft_array(self) -> np.ndarray:
+        a = np.zeros((self.B, max(self.k_max, 1)), np.int32)
+        for b, d in enumerate(self.drafts):
+            a[b, : len(d)] = d
+        return a
+
+    def draft_lens(self) -> np.ndarray:
+        return np.array([len(d) for d in self.drafts], np.int32)
+
+    def rows(self) -> int:
+        return int(sum(len(d) + 1 for d in self.drafts))
+
+
+class DeviceStep:
+    """Device copies of a Step plus output buffers."""
+
+    def __init__(self, st: Step, device="cuda", with_logits: bool = False, vocab: int = 0):
+        t = lambda a: torch.as_tensor(np.asarray(a), dtype=torch.int32).to(device)
+        self.step = st
+        self.seq = t(st.seq_ids)
+        self.ctx = t(st.ctx_lens)
+        self.last = t(st.last_tokens)
+        self.drafts = t(st.draft_array())
+        self.dlens = t(st.draft_lens())
+        self.accept = torch.zeros(st.B, dtype=torch.int32, device=device)
+        self.next = torch.zeros(st.B, dtype=torch.int32, device=device)
+        self.discard = torch.full((st.B,), -1, dtype=torch.int32, device=device)
+        self.logits = (torch.empty((st.B * (st.k_max + 1), vocab), dtype=torch.float32, device=device)
+                       if with_logits else None)
+
+    def verify(self, model: war.Model, pool: war.Pool, logits: bool = False):
+        war.verify_step(model, pool, self.seq, self.ctx, self.last, self.drafts, self.dlens,
+                        self.step.k_max, self.accept, self.next, self.logits if logits else None)
+
+    def commit(self, pool: war.Pool, discard: bool = True):
+        war.kv_commit(pool, self.seq, self.ctx, self.discard if discard else self.accept)
+
+
+def make_pool(cfg: synth.ModelConfig, ctx_lens, k_max: int, extra_pages: int = 64,
+              max_seqs: Optional[int] = None) -> war.Pool:
+    P = cfg.page_size
+    need = sum(cdiv(int(c) + k_max + 1, P) for c in ctx_lens) + extra_pages
+    max_pages = cdiv(int(max(ctx_lens)) + max(k_max, 64) + 1, P)
+    return war.Pool(cfg, need, max_seqs or len(ctx_lens), max_pages)
+
+
+def load_contexts(pool: war.Pool, cfg: synth.ModelConfig, ctx_lens, seq_ids, kv_seed: int,
+                  kv_keys=None) -> None:
+    """Reserve and fill each sequence's cached context with seeded keys/values."""
+    pool.alloc([int(s) for s in seq_ids], [int(c) for c in ctx_lens])
+    for i, (s, c) in enumerate(zip(seq_ids, ctx_lens)):
+        key = int(kv_keys[i]) if kv_keys is not None else int(s)
+        for l in range(cfg.n_layers):
+            pool.load(int(s), l, 0, synth.kv_context(cfg, kv_seed, key, l, 0, int(c), "cuda"))
+    torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------------ workloads
+def low_load_tokens(seed: int = 2, B: int = 8, ctx: int = 32768, n_prior: int = 64,
+                    prior_len: int = 32768, vocab: int = 151936):
+    """Motif-built contexts (+1 pending token each) and prior trajectories."""
+    bank = synth.MotifBank(seed, vocab)
+    contexts = [bank.trajectory(seed * 1000 + b, ctx + 1, end_mid_motif=(b % 2 == 0)) for b in range(B)]
+    prior = [bank.trajectory(seed * 1000 + 500 + i, prior_len) for i in range(n_prior)]
+    return contexts, prior
+
+
+def low_load_step(seed: int = 2, B: int = 8, ctx: int = 32768, k: int = 8, n_prior: int = 64,
+                  vocab: int = 151936, siblings: Optional[List[List[int]]] = None) -> Step:
+    contexts, prior = low_load_tokens(seed, B, ctx, n_prior, ctx, vocab)
+    d = SuffixDrafter()
+    for p in prior:
+        d.add_trajectory(p)
+    if siblings is not None:
+        # a sibling rollout that already produced this continuation (GRPO siblings)
+        for b in range(B):
+            d.add_trajectory(np.concatenate([contexts[b][-64:], siblings[b]]))
+    drafts = [d.propose(contexts[b], k) for b in range(B)]
+    return Step(np.arange(B, dtype=np.int32), np.full(B, ctx, np.int32),
+                np.array([c[-1] for c in contexts], np.int32), drafts, k)
+
+
+def high_load_step(seed: int = 0, B: int = 64, k: int = 0, vocab: int = 151936,
+                   drafts: Optional[List[List[int]]] = None) -> Step:
+    ctx = synth.lognormal_contexts(seed, B).astype(np.int32)
+    last = synth.uniform_tokens(seed + 77, B, vocab)
+    return Step(np.arange(B, dtype=np.int32), ctx, last, drafts or [[] for _ in range(B)], k)
+
+
+def teacher_continuation(model: war.Model, pool: war.Pool, st: Step, n: int) -> List[List[int]]:
+    """The target's own greedy continuation of each request (n tokens after the
+    pending token), by n verify steps that feed back the known prefix and
+    discard: the state of the pool is unchanged afterwards."""
+    cont: List[List[int]] = [[] for _ in range(st.B)]
+    for j in range(n):
+        s = Step(st.seq_ids, st.ctx_lens, st.last_tokens, [c[:j] for c in cont], max(j, 1))
+        ds = DeviceStep(s)
+        ds.verify(model, pool)
+        ds.commit(pool, discard=True)
+        nxt = ds.next.cpu().numpy()
+        acc = ds.accept.cpu().numpy()
+        for b in range(st.B):
+            assert acc[b] == j
+            cont[b].append(int(nxt[b]))
+    return cont
+
+
+def corrupt(drafts: List[List[int]], p: float, seed: int, vocab: int) -> List[List[int]]:
+    mask = synth.bernoulli_mask(seed, (len(drafts), max(len(d) for d in drafts)), p)
+    rng = np.random.default_rng([seed, 41])
+    out = []
+    for b, d in enumerate(drafts):
+        out.append([int((x + 1 + rng.integers(vocab - 1)) % vocab) if mask[b, i] else int(x)
+                    for i, x in enumerate(d)])
+    return out
+
+
+def step_kv_bytes(cfg: synth.ModelConfig, st: Step) -> int:
+    """KV bytes one layer's attention must read: every visible key and value."""
+    per_tok = 2 * cfg.n_kv_heads * cfg.head_dim * 2
+    return int(sum(int(c) + len(d) + 1 for c, d in zip(st.ctx_lens, st.drafts))) * per_tok
+
+
+def step_bytes(cfg: synth.ModelConfig, st: Step, logits: bool = False) -> int:
+    """Algorithmic HBM bytes of one verify step: streamed weights, KV read and
+    KV written (every layer), logits if written."""
+    kv_tok = cfg.kv_bytes_per_token()
+    T = st.rows()
+    b = cfg.streamed_weight_bytes() + cfg.n_layers * step_kv_bytes(cfg, st) + T * kv_tok
+    if logits:
+        b += 4 * T * cfg.vocab
+    return b

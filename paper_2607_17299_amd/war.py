@@ -26,7 +26,8 @@ _ERRORS = {-1: "WAR_ERR_INVALID_ARG", -2: "WAR_ERR_OUT_OF_PAGES", -3: "WAR_ERR_H
 EXPORTS = ["war_weight_count", "war_model_create", "war_model_destroy", "war_kv_pool_create",
            "war_kv_pool_destroy", "war_kv_alloc", "war_kv_fork", "war_kv_free", "war_kv_load",
            "war_prefill_append", "war_verify_step", "war_kv_commit", "war_pool_state",
-           "war_last_error", "war_debug_mfma16", "war_debug_workspace"]
+           "war_last_error", "war_debug_mfma16", "war_debug_workspace", "war_profile",
+           "war_profile_read"]
 
 
 class WarError(RuntimeError):
@@ -64,6 +65,8 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         "war_last_error": (C.c_char_p, []),
         "war_debug_mfma16": (i32, [vp, vp, vp, vp]),
         "war_debug_workspace": (i32, [vp, C.c_char_p, C.POINTER(vp), C.POINTER(C.c_int64)]),
+        "war_profile": (i32, [vp, i32]),
+        "war_profile_read": (i32, [vp, C.c_char_p, i32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(lib, name)
@@ -251,3 +254,18 @@ def debug_workspace(model: Model, name: str, dtype: torch.dtype, shape) -> torch
     hip = ctypes.CDLL("libamdhip64.so")
     hip.hipMemcpy(C.c_void_p(buf.data_ptr()), p, C.c_size_t(nbytes), 3)   # device to device
     return buf.view(dtype).view(*shape).clone()
+
+
+def profile(model: Model, enable: bool) -> None:
+    _check(lib().war_profile(model.handle, 1 if enable else 0))
+
+
+def profile_read(model: Model) -> Dict[str, tuple]:
+    """{kernel name: (calls, total_ms)} since the last read; synchronises."""
+    buf = C.create_string_buffer(1 << 16)
+    _check(lib().war_profile_read(model.handle, buf, len(buf)))
+    out = {}
+    for line in buf.value.decode().splitlines():
+        name, calls, ms = line.split()
+        out[name] = (int(calls), float(ms))
+    return out

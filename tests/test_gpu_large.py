@@ -1,0 +1,185 @@
+"""GPU parity on the 36-layer decoder's shapes (d 4096, 32 q / 8 kv heads,
+head_dim 128, FFN 12288, vocab 151936).
+
+* Reduced depth (2 layers, every width and the full vocabulary) against the
+  oracle on every request: ragged draft lengths covering all three query-row
+  tilings (k = 0, 2, 4, 8), contexts that are not multiples of a page or of
+  an attention chunk, and the multi-chunk split-KV path.
+* Prefill-append on the same shapes, then a verify step on the appended KV.
+* The full 36-layer low-load workload exactly as the benchmark runs it (8 x
+  32768 cached tokens, k = 8), checked on a sampled request.
+The cached contexts come from the seeded generator (an input of the step), so
+the oracle reads the very same keys and values.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle.decoder import RequestKV, Weights, forward_block
+from oracle.verify import prefill_request, verify_request
+from paper_2607_17299_amd import harness, synth
+from parity import compare_request
+
+pytestmark = pytest.mark.gpu
+KV_SEED = 9
+
+
+def _war():
+    from paper_2607_17299_amd import war
+    return war
+
+
+@pytest.fixture(scope="module")
+def large2():
+    war = _war()
+    cfg = synth.reduced(synth.LARGE, 2)
+    w = harness.large_weights(cfg)
+    model = war.Model(cfg, w, max_rows=512)
+    return {"cfg": cfg, "w": w, "model": model, "W": Weights(cfg, w), "war": war}
+
+
+def _oracle_kv(cfg, seq, ctx):
+    def get(l):
+        a = synth.kv_context(cfg, KV_SEED, seq, l, 0, ctx, "cuda").cpu().double().numpy()
+        return a[0], a[1]
+    return get
+
+
+def _check_step(env, st, report, tag):
+    cfg, model, W = env["cfg"], env["model"], env["W"]
+    pool = harness.make_pool(cfg, st.ctx_lens, st.k_max + 2)
+    harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, KV_SEED)
+    ds = harness.DeviceStep(st, with_logits=True, vocab=cfg.vocab)
+    ds.verify(model, pool, logits=True)
+    ds.commit(pool, discard=False)
+    torch.cuda.synchronize()
+    glog = ds.logits.cpu().numpy().reshape(st.B, st.k_max + 1, cfg.vocab)
+    acc, nxt = ds.accept.cpu().numpy(), ds.next.cpu().numpy()
+    errs = []
+    for b in range(st.B):
+        ctx = int(st.ctx_lens[b])
+        kv = RequestKV(cfg, [_oracle_kv(cfg, int(st.seq_ids[b]), ctx)(l) for l in range(cfg.n_layers)])
+        r = verify_request(cfg, W, kv, int(st.last_tokens[b]), st.drafts[b])
+        errs.append(compare_request(r["logits"], glog[b], st.drafts[b], r["accept"], r["next"],
+                                    int(acc[b]), int(nxt[b]), report, f"{tag} req {b}")["err"])
+        # the committed KV of the new rows matches the oracle's
+        keep = int(acc[b]) + 1
+        g = pool.gather_kv(int(st.seq_ids[b]), ctx + keep, cfg.n_layers - 1).double().cpu().numpy()
+        nk, nv = r["new_kv"][cfg.n_layers - 1]
+        np.testing.assert_allclose(g[0][:, ctx:], nk[:, :keep], atol=3e-2, rtol=2e-2)
+        np.testing.assert_allclose(g[1][:, ctx:], nv[:, :keep], atol=3e-2, rtol=2e-2)
+    got_ctx = ds.ctx.cpu().numpy()
+    np.testing.assert_array_equal(got_ctx, st.ctx_lens + acc + 1)
+    return max(errs)
+
+
+@pytest.mark.parametrize("k,lens,ctxs", [
+    (0, [0, 0, 0], [1000, 2500, 4097]),
+    (2, [2, 0, 1], [700, 3001, 1024]),
+    (4, [4, 1, 3], [1500, 33, 2048]),
+    (8, [8, 5, 0], [3000, 1100, 2500]),
+])
+def test_reduced_depth_verify_matches_oracle(large2, k, lens, ctxs):
+    cfg = large2["cfg"]
+    B = len(ctxs)
+    rng = np.random.default_rng(k)
+    drafts = [rng.integers(0, cfg.vocab, n).tolist() for n in lens]
+    st = harness.Step(np.arange(B, dtype=np.int32), np.array(ctxs, np.int32),
+                      synth.uniform_tokens(k + 40, B, cfg.vocab), drafts, k)
+    report = []
+    err = _check_step(large2, st, report, f"k={k}")
+    print(f"\nk={k}: max logit err {err:.3e}; reported {report}")
+
+
+def test_reduced_depth_sibling_drafts_accepted(large2):
+    """Drafts = the oracle's own greedy continuation (decisive LM head) are
+    accepted in full on the GPU."""
+    war = large2["war"]
+    cfg = large2["cfg"]
+    w = harness.large_weights(cfg, lm_std=0.2)
+    model = war.Model(cfg, w, max_rows=64)
+    W = Weights(cfg, w)
+    ctxs = np.array([1200, 2000], np.int32)
+    last = synth.uniform_tokens(61, 2, cfg.vocab)
+    k = 4
+    drafts = []
+    for b in range(2):
+        kv = RequestKV(cfg, [_oracle_kv(cfg, b, int(ctxs[b]))(l) for l in range(cfg.n_layers)])
+        toks, x = [], int(last[b])
+        for _ in range(k + 1):
+            r = verify_request(cfg, W, kv, x, [])
+            kv.append(r["new_kv"], 1)
+            x = r["next"]
+            toks.append(x)
+        drafts.append(toks)
+    st = harness.Step(np.arange(2, dtype=np.int32), ctxs, last, [d[:k] for d in drafts], k)
+    pool = harness.make_pool(cfg, st.ctx_lens, k + 2)
+    harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, KV_SEED)
+    ds = harness.DeviceStep(st)
+    ds.verify(model, pool)
+    ds.commit(pool, discard=False)
+    assert ds.accept.cpu().tolist() == [k, k]
+    assert ds.next.cpu().tolist() == [d[k] for d in drafts]
+
+
+def test_reduced_depth_prefill_append(large2):
+    war, cfg, model, W = large2["war"], large2["cfg"], large2["model"], large2["W"]
+    ctxs = np.array([512, 96], np.int32)
+    n_new = [300, 45]
+    pool = harness.make_pool(cfg, ctxs + np.array(n_new), 8)
+    harness.load_contexts(pool, cfg, ctxs, [0, 1], KV_SEED)
+    toks = [synth.uniform_tokens(70 + b, n, cfg.vocab) for b, n in enumerate(n_new)]
+    t = lambda a: torch.as_tensor(np.asarray(a), dtype=torch.int32).cuda()
+    ctx_d = t(ctxs)
+    nxt = t([0, 0])
+    last = torch.zeros((2, cfg.vocab), device="cuda")
+    war.prefill_append(model, pool, t([0, 1]), ctx_d, n_new, t(np.concatenate(toks)), nxt, last)
+    assert ctx_d.cpu().tolist() == (ctxs + np.array(n_new)).tolist()
+    gl = last.cpu().numpy()
+    for b in range(2):
+        kv = RequestKV(cfg, [_oracle_kv(cfg, b, int(ctxs[b]))(l) for l in range(cfg.n_layers)])
+        r = prefill_request(cfg, W, kv, toks[b])
+        err = np.abs(gl[b] - r["logits"][-1]).max()
+        assert err < 5e-2, err
+        if int(nxt[b]) != r["next"]:
+            s = np.sort(r["logits"][-1])
+            assert s[-1] - s[-2] <= 2 * err
+        g = pool.gather_kv(b, int(ctxs[b]) + n_new[b], 1).double().cpu().numpy()
+        K, V = kv.get(1)
+        np.testing.assert_allclose(g[0][:, ctxs[b]:], K[:, ctxs[b]:], atol=3e-2, rtol=2e-2)
+        np.testing.assert_allclose(g[1][:, ctxs[b]:], V[:, ctxs[b]:], atol=3e-2, rtol=2e-2)
+
+
+def test_full_size_low_load_sampled():
+    """The benchmark's workload at full size (36 layers, 8 x 32768, k = 8), with
+    logits; request 0 is recomputed by the oracle, layer by layer."""
+    war = _war()
+    cfg = synth.LARGE
+    w = harness.large_weights(cfg)
+    model = war.Model(cfg, w, max_rows=1024)
+    st = harness.low_load_step()
+    pool = harness.make_pool(cfg, st.ctx_lens, st.k_max + 8)
+    harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, 5)
+    ds = harness.DeviceStep(st, with_logits=True, vocab=cfg.vocab)
+    ds.verify(model, pool, logits=True)
+    ds.commit(pool, discard=True)
+    torch.cuda.synchronize()
+    glog = ds.logits.cpu().numpy().reshape(st.B, st.k_max + 1, cfg.vocab)
+    acc, nxt = ds.accept.cpu().numpy(), ds.next.cpu().numpy()
+    assert np.isfinite(glog[:, 0]).all()
+    W = Weights(cfg, w, cache=False)
+    b = 0
+    ctx = int(st.ctx_lens[b])
+
+    def kv_get(l):
+        a = synth.kv_context(cfg, 5, int(st.seq_ids[b]), l, 0, ctx, "cuda").cpu().double().numpy()
+        return a[0], a[1]
+    tokens = [int(st.last_tokens[b])] + st.drafts[b]
+    logits, _ = forward_block(cfg, W, tokens, ctx, kv_get)
+    from oracle.accept import accept_length, argmax_lowest
+    g = argmax_lowest(logits)
+    a = accept_length(st.drafts[b], g)
+    report = []
+    s = compare_request(logits, glog[b], st.drafts[b], a, int(g[a]), int(acc[b]), int(nxt[b]),
+                        report, "full req 0")
+    print(f"\nfull size: max logit err {s['err']:.3e}, min oracle gap {s['min_gap']:.3g}; {report}")
