@@ -31,15 +31,29 @@ __device__ __forceinline__ uint4 keep_first(uint4 v, int n) {
   return make_uint4(v.x & m(0), v.y & m(1), v.z & m(2), v.w & m(3));
 }
 
-template <int NR, int HD>
-__global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
+// K and V^T fragments of one 32-key block (see the file comment for the layout).
+template <int HD>
+struct KVFrag {
+  uint4 k[2][HD / 32];
+  uint4 v[HD / 16];
+};
+
+// DEPTH = blocks in flight per wave beyond the one being computed (0, 1 or 2);
+// QLDS = queries read from LDS instead of registers; WPE = waves per SIMD the
+// register budget allows.  Two waves per SIMD let one wave's MFMA/softmax work
+// overlap the other's memory waits.
+template <int NR, int HD, int DEPTH, bool QLDS, int WPE>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
+k_attn(AttnArgs a) {
   constexpr int DPL = HD / 4;    // dims per lane group in the S^T operands
   constexpr int KSUB = HD / 32;  // MFMA k-steps over the head dim
   constexpr int NDT = HD / 16;   // 16-dim output tiles
   constexpr int RB = NR * 16;
   constexpr int OST = HD + 1;    // LDS row stride of the merge buffer
+  constexpr int QST = HD + 8;    // LDS row stride (bf16) of the staged queries
   __shared__ float s_m[4][RB], s_l[4][RB];
   __shared__ float s_o[RB * OST];
+  __shared__ __attribute__((aligned(16))) bf16_t s_q[QLDS ? RB * QST : 8];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
   const int total = a.meta.n_items[0] * a.n_kv_heads;
   const int P = a.kv.page_size;
@@ -60,22 +74,44 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
 
     // queries (B operand of S^T): lane (n = ln, g = lg) of row tile rt
     int rpos[NR];
-    bf16x8 qf[NR][KSUB];
+    bf16x8 qf[QLDS ? 1 : NR][KSUB];
 #pragma unroll
     for (int rt = 0; rt < NR; ++rt) {
       const int r = rt * 16 + ln;
-      if (r < nrows) {
-        const int ti = t0 + r / a.G, h = kvh * a.G + r % a.G;
-        rpos[rt] = pos0 + ti;
-        const bf16_t* qp = a.q + (int64_t)(row0 + ti) * a.q_stride + h * HD + lg * DPL;
+      rpos[rt] = r < nrows ? pos0 + t0 + r / a.G : last_pos;
+    }
+    if constexpr (QLDS) {
+      for (int e = tid; e < RB * (HD / 8); e += 256) {
+        const int r = e / (HD / 8), c = (e % (HD / 8)) * 8;
+        uint4 v = make_uint4(0, 0, 0, 0);
+        if (r < nrows) {
+          const int ti = t0 + r / a.G, h = kvh * a.G + r % a.G;
+          v = *reinterpret_cast<const uint4*>(a.q + (int64_t)(row0 + ti) * a.q_stride + h * HD + c);
+        }
+        *reinterpret_cast<uint4*>(&s_q[r * QST + c]) = v;
+      }
+      __syncthreads();
+    } else {
 #pragma unroll
-        for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + j * 8));
-      } else {
-        rpos[rt] = last_pos;
+      for (int rt = 0; rt < (QLDS ? 1 : NR); ++rt) {
+        const int r = rt * 16 + ln;
+        if (r < nrows) {
+          const int ti = t0 + r / a.G, h = kvh * a.G + r % a.G;
+          const bf16_t* qp = a.q + (int64_t)(row0 + ti) * a.q_stride + h * HD + lg * DPL;
 #pragma unroll
-        for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(make_uint4(0, 0, 0, 0));
+          for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + j * 8));
+        } else {
+#pragma unroll
+          for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(make_uint4(0, 0, 0, 0));
+        }
       }
     }
+    auto qfrag = [&](int rt, int j) -> bf16x8 {
+      if constexpr (QLDS)
+        return as_bf16x8(*reinterpret_cast<const uint4*>(&s_q[(rt * 16 + ln) * QST + lg * DPL + j * 8]));
+      else
+        return qf[rt][j];
+    };
 
     float m_run[NR], l_run[NR];
     f32x4 o_acc[NDT][NR];
@@ -89,13 +125,11 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
 
     const int CW = a.chunk / 4;
     const int wk0 = kbeg + w * CW, wk1 = min(kend, wk0 + CW);
+    const int nb = wk1 > wk0 ? (wk1 - wk0 + 31) / 32 : 0;
     const int32_t* trow = a.table + (int64_t)seq * a.max_pages;
     const bf16_t* kvl = a.kv.kv;
 
-    // K fragments (A operand, lane (m = ln, g = lg)) and V^T fragments (A operand of
-    // the second product, lane (m = dim, g = lg) -> keys lg*8..+7) of a 32-key block
-    uint4 kf[2][KSUB], vf[NDT];
-    auto load_block = [&](int kb) {
+    auto load_block = [&](KVFrag<HD>& f, int kb) {
       const int pg0 = trow[kb / P];
       const int pg1 = (kb + 16 < S) ? trow[kb / P + 1] : pg0;
 #pragma unroll
@@ -104,42 +138,45 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
         const int pg = kk < 16 ? pg0 : pg1;
         const bf16_t* kp = kvl + a.kv.page_elems(a.layer, pg, kvh, 0) + (kk & 15) * HD + lg * DPL;
 #pragma unroll
-        for (int j = 0; j < KSUB; ++j) kf[t][j] = *reinterpret_cast<const uint4*>(kp + j * 8);
+        for (int j = 0; j < KSUB; ++j) f.k[t][j] = *reinterpret_cast<const uint4*>(kp + j * 8);
       }
       const int pg = lg < 2 ? pg0 : pg1;
       const bf16_t* vp = kvl + a.kv.page_elems(a.layer, pg, kvh, 1) + (lg & 1) * 8;
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) vf[dt] = *reinterpret_cast<const uint4*>(vp + (dt * 16 + ln) * P);
+      for (int dt = 0; dt < NDT; ++dt) f.v[dt] = *reinterpret_cast<const uint4*>(vp + (dt * 16 + ln) * P);
       if (kb + 32 > S) {  // the sequence ends inside this block
         const int nvalid = min(max(S - (kb + lg * 8), 0), 8);
 #pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) vf[dt] = keep_first(vf[dt], nvalid);
+        for (int dt = 0; dt < NDT; ++dt) f.v[dt] = keep_first(f.v[dt], nvalid);
       }
     };
 
-    if (wk0 < wk1) load_block(wk0);
-    for (int kb = wk0; kb < wk1; kb += 32) {
-      bf16x8 kc[2][KSUB], vc[NDT];
-#pragma unroll
-      for (int t = 0; t < 2; ++t)
-#pragma unroll
-        for (int j = 0; j < KSUB; ++j) kc[t][j] = as_bf16x8(kf[t][j]);
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) vc[dt] = as_bf16x8(vf[dt]);
-      if (kb + 32 < wk1) load_block(kb + 32);  // in flight while this block computes
-
+    auto compute_block = [&](const KVFrag<HD>& f, int kb) {
       // keys of this block above the smallest row position need the causal mask
       const bool tail = kb + 31 > pos0 + t0;
+      if constexpr (QLDS) asm volatile("" ::: "memory");  // re-read Q from LDS each block
+      // phase 1: scores of every row tile (the K fragments die after this)
+      float sc[NR][8];
 #pragma unroll
       for (int rt = 0; rt < NR; ++rt) {
         f32x4 s0 = {0.f, 0.f, 0.f, 0.f}, s1 = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int j = 0; j < KSUB; ++j) {
-          s0 = mfma16(kc[0][j], qf[rt][j], s0);
-          s1 = mfma16(kc[1][j], qf[rt][j], s1);
+          const bf16x8 q = qfrag(rt, j);
+          s0 = mfma16(as_bf16x8(f.k[0][j]), q, s0);
+          s1 = mfma16(as_bf16x8(f.k[1][j]), q, s1);
         }
         // lane holds S^T[key kb + lg*8 + 4t + i][row rt*16 + ln]
-        float sv[8] = {s0[0], s0[1], s0[2], s0[3], s1[0], s1[1], s1[2], s1[3]};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          sc[rt][i] = s0[i];
+          sc[rt][4 + i] = s1[i];
+        }
+      }
+      // phase 2: online softmax and O^T += V^T P^T per row tile
+#pragma unroll
+      for (int rt = 0; rt < NR; ++rt) {
+        float* sv = sc[rt];
         if (tail) {
 #pragma unroll
           for (int e = 0; e < 8; ++e)
@@ -181,8 +218,45 @@ __global__ void __launch_bounds__(256) k_attn(AttnArgs a) {
         const bf16x8 pl = as_bf16x8(make_uint4(lo[0], lo[1], lo[2], lo[3]));
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-          o_acc[dt][rt] = mfma16(vc[dt], ph, o_acc[dt][rt]);
-          o_acc[dt][rt] = mfma16(vc[dt], pl, o_acc[dt][rt]);
+          o_acc[dt][rt] = mfma16(as_bf16x8(f.v[dt]), ph, o_acc[dt][rt]);
+          o_acc[dt][rt] = mfma16(as_bf16x8(f.v[dt]), pl, o_acc[dt][rt]);
+        }
+      }
+    };
+
+    // Block i of this wave is at key wk0 + 32 i; blocks in flight rotate through
+    // DEPTH + 1 register sets (static indexing: the loop is unrolled by DEPTH + 1).
+    if constexpr (DEPTH == 0) {
+      KVFrag<HD> f0;
+      for (int i = 0; i < nb; ++i) {
+        load_block(f0, wk0 + 32 * i);
+        compute_block(f0, wk0 + 32 * i);
+      }
+    } else if constexpr (DEPTH == 1) {
+      KVFrag<HD> f0, f1;
+      if (nb > 0) load_block(f0, wk0);
+      for (int i = 0; i < nb; i += 2) {
+        if (i + 1 < nb) load_block(f1, wk0 + 32 * (i + 1));
+        compute_block(f0, wk0 + 32 * i);
+        if (i + 1 < nb) {
+          if (i + 2 < nb) load_block(f0, wk0 + 32 * (i + 2));
+          compute_block(f1, wk0 + 32 * (i + 1));
+        }
+      }
+    } else {
+      KVFrag<HD> f0, f1, f2;
+      if (nb > 0) load_block(f0, wk0);
+      if (nb > 1) load_block(f1, wk0 + 32);
+      for (int i = 0; i < nb; i += 3) {
+        if (i + 2 < nb) load_block(f2, wk0 + 32 * (i + 2));
+        compute_block(f0, wk0 + 32 * i);
+        if (i + 1 < nb) {
+          if (i + 3 < nb) load_block(f0, wk0 + 32 * (i + 3));
+          compute_block(f1, wk0 + 32 * (i + 1));
+        }
+        if (i + 2 < nb) {
+          if (i + 4 < nb) load_block(f1, wk0 + 32 * (i + 4));
+          compute_block(f2, wk0 + 32 * (i + 2));
         }
       }
     }
@@ -302,12 +376,17 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   }
 }
 
+// Tuned per row-tile count: one tile prefetches one block and keeps Q in
+// registers; two or three tiles keep Q in LDS and no prefetch buffer so that
+// two waves fit each SIMD.
 template <int NR>
 void launch_attn_nr(const AttnArgs& a, int head_dim, int grid, hipStream_t st) {
+  constexpr int DEPTH = NR == 1 ? 1 : 0;
+  constexpr bool QLDS = NR > 1;
   if (head_dim == 128)
-    k_attn<NR, 128><<<grid, 256, 0, st>>>(a);
+    k_attn<NR, 128, DEPTH, QLDS, 2><<<grid, 256, 0, st>>>(a);
   else
-    k_attn<NR, 64><<<grid, 256, 0, st>>>(a);
+    k_attn<NR, 64, DEPTH, QLDS, 2><<<grid, 256, 0, st>>>(a);
 }
 
 template <int RB>

@@ -685,8 +685,8 @@ war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_
   const int kp1 = k_max + 1;
   const int R = B * kp1;
   const int RB = attn_rows_per_block(G, kp1);
-  int chunk = 256;
-  while (chunk < 2048 && chunk * 2 <= G * kp1 * 32) chunk *= 2;
+  // keys per attention item: long enough that each wave streams 8+ blocks
+  int chunk = 1024;
   while (cdiv_i(p->dev.max_pages * P, chunk) > kMaxItemsPerSeq) chunk *= 2;
   const int64_t max_items = (int64_t)B * cdiv_i(p->dev.max_pages * P, chunk);
   war_status s = ensure_items(m, max_items, RB);
@@ -708,7 +708,8 @@ war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_
   }
 
   AttnArgs a = attn_args(m, p, kp1, chunk);
-  const int grid = (int)std::min<int64_t>(max_items * m->md.nkv, RB == 48 ? 1024 : 2048);
+  // persistent grid = resident capacity: 2 workgroups per CU
+  const int grid = (int)std::min<int64_t>(max_items * m->md.nkv, 512);
   s = run_layers(m, p, R, a, RB, grid, B, st);
   if (s != WAR_OK) return s;
   int sdummy;
@@ -861,7 +862,7 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
     HIPCHK(hipStreamSynchronize(st));  // host vectors go out of scope below
 
     AttnArgs a = attn_args(m, p, TB, chunk);
-    const int grid = (int)std::min<int64_t>((int64_t)ni * m->md.nkv, 2048);
+    const int grid = (int)std::min<int64_t>((int64_t)ni * m->md.nkv, 512);
     s = run_layers(m, p, R, a, RB, std::max(grid, 1), nseg, st);
     if (s != WAR_OK) return s;
     // LM head on the rows that end a sequence inside this chunk
