@@ -20,6 +20,12 @@ output, the SwiGLU product) and the rotated q, k and the v of the new tokens
 statistics, rotation, softmax, logits) stays float64.  ``rounding=False`` gives
 the pure float64 decoder.
 
+``precision="fp32"`` runs every matrix product and the attention in float32
+(same rounding points).  It is the same algorithm at the accumulation
+precision of a bf16 kernel, used to measure how far any fp32-accumulating
+implementation drifts from the float64 result (the parity tolerance at full
+depth is derived from that drift).
+
 The verify step scores all new tokens of a request in ONE forward pass with a
 causal mask inside the block (System Design, "SuffixDecoding": drafts verified
 by the target in a single forward pass).
@@ -94,13 +100,13 @@ def attention(q: np.ndarray, K: np.ndarray, V: np.ndarray, q_pos: np.ndarray,
     """q [n, Hq, D]; K, V [Hkv, S, D] hold keys/values at positions 0..S-1.
 
     Query i (position q_pos[i]) of head h attends keys 0..q_pos[i] of kv-head
-    h // group.  Returns o [n, Hq, D] float64.
+    h // group.  Returns o [n, Hq, D] in the inputs' float type.
     """
     n, Hq, D = q.shape
     S = K.shape[1]
-    scale = 1.0 / np.sqrt(D)
+    scale = q.dtype.type(1.0 / np.sqrt(D))
     visible = np.arange(S)[None, :] <= np.asarray(q_pos)[:, None]      # [n, S]
-    o = np.empty((n, Hq, D), dtype=np.float64)
+    o = np.empty((n, Hq, D), dtype=q.dtype)
     for h in range(Hq):
         g = h // group
         s = (q[:, h, :] @ K[g].T) * scale                                # [n, S]
@@ -116,7 +122,7 @@ KVGetter = Callable[[int], Tuple[np.ndarray, np.ndarray]]
 
 
 def forward_block(cfg, W: Weights, tokens: Sequence[int], pos0: int, kv_get: KVGetter,
-                  rounding: bool = True, want_logits: bool = True):
+                  rounding: bool = True, want_logits: bool = True, precision: str = "fp64"):
     """Run tokens (at positions pos0, pos0+1, ...) through the decoder.
 
     ``kv_get(l)`` returns the cached keys and values of layer l for positions
@@ -125,6 +131,15 @@ def forward_block(cfg, W: Weights, tokens: Sequence[int], pos0: int, kv_get: KVG
     = (K_new [Hkv, n, D], V_new [Hkv, n, D]) for the block's own tokens.
     """
     rb = round_bf16 if rounding else (lambda a: a)
+    if precision == "fp64":
+        mm = lambda x, Wt: x @ Wt.T
+        attn = attention
+    elif precision == "fp32":
+        f32 = lambda a: np.asarray(a, dtype=np.float32)
+        mm = lambda x, Wt: (f32(x) @ f32(Wt).T).astype(np.float64)
+        attn = lambda q, K, V, p, g: attention(f32(q), f32(K), f32(V), p, g).astype(np.float64)
+    else:
+        raise ValueError(precision)
     n = len(tokens)
     Hq, Hkv, D = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     pos = pos0 + np.arange(n)
@@ -133,7 +148,7 @@ def forward_block(cfg, W: Weights, tokens: Sequence[int], pos0: int, kv_get: KVG
     for l in range(cfg.n_layers):
         p = f"l{l}."
         u = rb(rms_norm(h, W.get(p + "attn_norm"), cfg.rms_eps))
-        qkv = u @ W.get(p + "w_qkv").T                                  # [n, qkv]
+        qkv = mm(u, W.get(p + "w_qkv"))                                 # [n, qkv]
         q = qkv[:, : Hq * D].reshape(n, Hq, D)
         k = qkv[:, Hq * D: (Hq + Hkv) * D].reshape(n, Hkv, D)
         v = qkv[:, (Hq + Hkv) * D:].reshape(n, Hkv, D)
@@ -144,15 +159,15 @@ def forward_block(cfg, W: Weights, tokens: Sequence[int], pos0: int, kv_get: KVG
         K = np.concatenate([Kc, k.transpose(1, 0, 2)], axis=1)          # [Hkv, pos0+n, D]
         V = np.concatenate([Vc, v.transpose(1, 0, 2)], axis=1)
         new_kv.append((k.transpose(1, 0, 2).copy(), v.transpose(1, 0, 2).copy()))
-        o = rb(attention(q, K, V, pos, Hq // Hkv)).reshape(n, Hq * D)
-        h = h + o @ W.get(p + "w_o").T
+        o = rb(attn(q, K, V, pos, Hq // Hkv)).reshape(n, Hq * D)
+        h = h + mm(o, W.get(p + "w_o"))
         u = rb(rms_norm(h, W.get(p + "ffn_norm"), cfg.rms_eps))
-        y = rb(silu(u @ W.get(p + "w_gate").T) * (u @ W.get(p + "w_up").T))
-        h = h + y @ W.get(p + "w_down").T
+        y = rb(silu(mm(u, W.get(p + "w_gate"))) * mm(u, W.get(p + "w_up")))
+        h = h + mm(y, W.get(p + "w_down"))
     hf = rb(rms_norm(h, W.get("final_norm"), cfg.rms_eps))
     if not want_logits:
         return hf, new_kv
-    return hf @ W.get("w_lm").T, new_kv
+    return mm(hf, W.get("w_lm")), new_kv
 
 
 class RequestKV:

@@ -28,9 +28,9 @@ from .decoder import RequestKV, Weights, forward_block
 
 
 def verify_request(cfg, W: Weights, kv: RequestKV, last_token: int, drafts: Sequence[int],
-                   rounding: bool = True) -> Dict:
+                   rounding: bool = True, precision: str = "fp64") -> Dict:
     tokens = [int(last_token)] + [int(d) for d in drafts]
-    logits, new_kv = forward_block(cfg, W, tokens, kv.length, kv.get, rounding)
+    logits, new_kv = forward_block(cfg, W, tokens, kv.length, kv.get, rounding, precision=precision)
     g = argmax_lowest(logits)
     a = accept_length(drafts, g)
     return {"logits": logits, "greedy": g, "accept": a, "next": int(g[a]), "new_kv": new_kv}

@@ -85,6 +85,18 @@ def test_float64_decoder_matches_transformers_llama(tiny_weights, W):
     assert stream == gen
 
 
+def test_float32_mode_matches_transformers_llama_in_float32(tiny_weights, W):
+    # the fp32-accumulation mode computes the same function at float32 precision
+    m = _hf_llama(tiny_weights).float()
+    toks = synth.uniform_tokens(15, 40, CFG.vocab)
+    ours, _ = forward_block(CFG, W, toks, 0, _empty, rounding=False, precision="fp32")
+    with torch.no_grad():
+        ref = m(torch.from_numpy(toks.astype(np.int64))[None]).logits[0].double().numpy()
+    np.testing.assert_allclose(ours, ref, atol=1e-4, rtol=0)
+    ours64, _ = forward_block(CFG, W, toks, 0, _empty, rounding=False)
+    assert 0 < np.abs(ours - ours64).max() < 1e-4
+
+
 def test_rounding_points_change_logits_only_at_bf16_scale(W):
     toks = synth.uniform_tokens(6, 32, CFG.vocab)
     a, _ = forward_block(CFG, W, toks, 0, _empty, rounding=False)
