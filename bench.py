@@ -86,9 +86,10 @@ def measured_traffic(workload: str):
     return rec["workloads"][workload]["traffic_bytes"]
 
 
-def cpu_baseline(cfg, weights, st, kv_seed):
-    """Time the oracle on 1 request: embedding + LM head alone, and with 2 of
-    the 36 layers; the per-request time is extrapolated to all layers."""
+def cpu_baseline(cfg, weights, st, kv_seed, sample_layers: int = 8):
+    """Time the oracle on 1 request: embedding + LM head alone, and with
+    `sample_layers` of the 36 layers; the per-request time is extrapolated to
+    all layers."""
     import numpy as np
     import threadpoolctl
     import torch
@@ -115,9 +116,10 @@ def cpu_baseline(cfg, weights, st, kv_seed):
     info = threadpoolctl.threadpool_info()
     threads = max([i.get("num_threads", 1) for i in info] or [1])
     t_head = run(0)
-    t_two = run(2)
-    t_req = t_head + (t_two - t_head) * cfg.n_layers / 2
-    return {"t_request_s": t_req, "threads": threads, "t_sample_s": t_head + t_two}
+    t_some = run(sample_layers)
+    t_req = t_head + (t_some - t_head) * cfg.n_layers / sample_layers
+    return {"t_request_s": t_req, "threads": threads, "t_sample_s": t_head + t_some,
+            "sample_layers": sample_layers}
 
 
 def main():
@@ -214,8 +216,9 @@ def main():
         # oracle throughput: the sampled request's accepted tokens over B sequential requests
         cpu = {"value": round(accepted / (st.B * c["t_request_s"]), 4), "unit": "accepted tokens/s",
                "cores": c["threads"], "kind": "oracle",
-               "sample": (f"request 0 of {st.B}: embedding + final norm + LM head, and 2 of 36 layers, "
-                          f"timed ({c['t_sample_s']:.1f}s); per-request time = head + 18 x (2-layer part) "
+               "sample": (f"request 0 of {st.B}: embedding + final norm + LM head alone, and with "
+                          f"{c['sample_layers']} of 36 layers, timed ({c['t_sample_s']:.1f}s in all); "
+                          f"per-request time = head + 36/{c['sample_layers']} x (layer part) "
                           f"= {c['t_request_s']:.1f}s; every request costs the same")}
 
     out = {

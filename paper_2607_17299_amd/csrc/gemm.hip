@@ -9,10 +9,13 @@
 // 16-wide MFMA n-tiles) and all MT 16-row m-tiles of the workgroup's m-block.
 // K advances in steps of 64:
 //   * W goes straight from HBM to registers -- each lane reads 32 contiguous
-//     bytes of two W rows per step (4 lanes cover a 128-byte line) -- with three
-//     steps in flight;
-//   * the A tile (MT*16 rows x 64) is staged through LDS (double-buffered,
-//     rows padded to 144 bytes) and shared by the 4 waves;
+//     bytes of two W rows per step (4 lanes cover a 128-byte line);
+//   * the A tile (MT*16 rows x 64) is loaded into registers by all 256 threads
+//     and staged through LDS (three buffers, rows padded to 144 bytes), shared
+//     by the 4 waves;
+//   * both are requested three steps ahead, A before W, so that the in-order
+//     memory counter never makes a step wait for loads younger than its own;
+//     the A tile of step s+1 goes to LDS at the end of step s (one barrier);
 //   * v_mfma_f32_16x16x32_bf16 accumulates in fp32.  Inside a step the
 //     k-index is permuted identically for A and W (lane group g holds k
 //     g*16 .. g*16+15), which leaves the dot products unchanged.
@@ -34,51 +37,61 @@ struct Tile {
   static constexpr int BYTES = MT * 16 * ROWB;
 };
 
-template <int MT, int EPI>
-__global__ void __launch_bounds__(256) k_gemm(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) unsigned char sA[2][Tile<MT>::BYTES];
+// NSTEPS > 0: every split covers exactly NSTEPS k-steps and the step loop is
+// fully unrolled (straight-line code lets the compiler's memory-counter waits
+// stay exact, so loads issued three steps ahead really stay in flight);
+// NSTEPS == 0: a runtime loop over (K split) / 64 steps.
+template <int MT, int NSTEPS, int EPI>
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm(GemmArgs g) {
+  __shared__ __attribute__((aligned(16))) unsigned char sA[3][Tile<MT>::BYTES];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
   const int split = blockIdx.y;
   const int m0 = blockIdx.z * MT * 16;
   const int kb = split * g.kper;
   const int ke = min(g.K, kb + g.kper);
-  const int nsteps = (ke - kb) / KS;
+  const int nsteps = NSTEPS > 0 ? NSTEPS : (ke - kb) / KS;
   const int n0 = blockIdx.x * 128;
   const bf16_t* Wb = n0 < g.n_split ? g.W1 + (int64_t)n0 * g.ldw
                                     : g.W2 + (int64_t)(n0 - g.n_split) * g.ldw;
-  const bf16_t* w0 = Wb + (int64_t)(w * 32 + ln) * g.ldw + kb + lg * 16;
-  const bf16_t* w1 = w0 + (int64_t)16 * g.ldw;
 
-  // A rows this thread stages (fixed across steps)
-  const bf16_t* arow[Tile<MT>::PER_THREAD];
+  // Loads are raw buffer loads (one descriptor for the W block, one for A): the
+  // compiler does not re-issue them next to their use, so they stay in flight
+  // for the steps in between.  A rows at or beyond M load row 0 instead (no
+  // per-lane branch around the load): an output row depends only on its own A
+  // row, and rows >= M are never written.
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  const __amdgpu_buffer_rsrc_t wres =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(Wb), 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ares =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(g.A), 0, 0x7fffffff, 0x00020000);
+  const int wv0 = ((w * 32 + ln) * g.ldw + kb + lg * 16) * 2;  // byte offsets
+  const int wv1 = wv0 + 16 * g.ldw * 2;
+  int av[Tile<MT>::PER_THREAD];
   int aoff[Tile<MT>::PER_THREAD];
 #pragma unroll
   for (int i = 0; i < Tile<MT>::PER_THREAD; ++i) {
-    const int c = tid + 256 * i;
+    const int c = min(tid + 256 * i, Tile<MT>::CHUNKS - 1);
     const int r = c >> 3, q = c & 7;
     const int gm = m0 + r;
-    arow[i] = nullptr;
     aoff[i] = r * ROWB + q * 16;
-    if (c < Tile<MT>::CHUNKS && gm < g.M) {
-      const int src = g.a_rows ? g.a_rows[gm] : gm;
-      arow[i] = g.A + (int64_t)src * g.lda + kb + q * 8;
-    }
+    const int src = gm < g.M ? (g.a_rows ? g.a_rows[gm] : gm) : (g.a_rows ? g.a_rows[0] : 0);
+    av[i] = (src * g.lda + kb + q * 8) * 2;
   }
 
+  auto bload = [](__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+  };
   auto load_w = [&](uint4* wr, int s) {
-    const int k = s * KS;
-    wr[0] = *reinterpret_cast<const uint4*>(w0 + k);
-    wr[1] = *reinterpret_cast<const uint4*>(w0 + k + 8);
-    wr[2] = *reinterpret_cast<const uint4*>(w1 + k);
-    wr[3] = *reinterpret_cast<const uint4*>(w1 + k + 8);
+    wr[0] = bload(wres, wv0, s * KS * 2);
+    wr[1] = bload(wres, wv0 + 16, s * KS * 2);
+    wr[2] = bload(wres, wv1, s * KS * 2);
+    wr[3] = bload(wres, wv1 + 16, s * KS * 2);
   };
-  uint4 ar[Tile<MT>::PER_THREAD];
-  auto load_a = [&](int s) {
+  auto load_a = [&](uint4* ar, int s) {
 #pragma unroll
-    for (int i = 0; i < Tile<MT>::PER_THREAD; ++i)
-      ar[i] = arow[i] ? *reinterpret_cast<const uint4*>(arow[i] + s * KS) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < Tile<MT>::PER_THREAD; ++i) ar[i] = bload(ares, av[i], s * KS * 2);
   };
-  auto store_a = [&](int buf) {
+  auto store_a = [&](const uint4* ar, int buf) {
 #pragma unroll
     for (int i = 0; i < Tile<MT>::PER_THREAD; ++i)
       if (tid + 256 * i < Tile<MT>::CHUNKS)
@@ -103,28 +116,42 @@ __global__ void __launch_bounds__(256) k_gemm(GemmArgs g) {
     }
   };
 
+  // register sets rotate with period 3: step s uses wr[s%3]; ar[s%3] holds A(s)
+  // until it is stored, then receives A(s+3)
   uint4 wA[4], wB[4], wC[4];
-  if (nsteps > 0) load_w(wA, 0);
-  if (nsteps > 1) load_w(wB, 1);
-  if (nsteps > 2) load_w(wC, 2);
-  if (nsteps > 0) {
-    load_a(0);
-    store_a(0);
-  }
+  uint4 aA[Tile<MT>::PER_THREAD], aB[Tile<MT>::PER_THREAD], aC[Tile<MT>::PER_THREAD];
+  if (nsteps > 0) { load_a(aA, 0); load_w(wA, 0); }
+  if (nsteps > 1) { load_a(aB, 1); load_w(wB, 1); }
+  if (nsteps > 2) { load_a(aC, 2); load_w(wC, 2); }
+  __builtin_amdgcn_sched_barrier(0);
+  if (nsteps > 0) store_a(aA, 0);
   __syncthreads();
 
-#define GEMM_STEP(WR, S)                         \
-  if ((S) < nsteps) {                            \
-    if ((S) + 1 < nsteps) load_a((S) + 1);       \
-    compute(WR, (S)&1);                          \
-    if ((S) + 3 < nsteps) load_w(WR, (S) + 3);   \
-    if ((S) + 1 < nsteps) store_a(((S) + 1) & 1); \
-    __syncthreads();                             \
+// sched_barrier pins the loads where they are issued: otherwise the scheduler
+// sinks each load next to its use and the step waits for it right away.
+#define GEMM_STEP(S, AL, AS, WR, B)                    \
+  if ((S) < nsteps) {                                  \
+    if ((S) + 3 < nsteps) load_a(AL, (S) + 3);         \
+    __builtin_amdgcn_sched_barrier(0);                 \
+    compute(WR, B);                                    \
+    if ((S) + 3 < nsteps) load_w(WR, (S) + 3);         \
+    __builtin_amdgcn_sched_barrier(0);                 \
+    if ((S) + 1 < nsteps) store_a(AS, ((B) + 1) % 3);  \
+    __syncthreads();                                   \
   }
-  for (int s = 0; s < nsteps; s += 3) {
-    GEMM_STEP(wA, s)
-    GEMM_STEP(wB, s + 1)
-    GEMM_STEP(wC, s + 2)
+  if constexpr (NSTEPS > 0) {
+#pragma unroll
+    for (int s = 0; s < NSTEPS; s += 3) {
+      GEMM_STEP(s, aA, aB, wA, 0)
+      GEMM_STEP(s + 1, aB, aC, wB, 1)
+      GEMM_STEP(s + 2, aC, aA, wC, 2)
+    }
+  } else {
+    for (int s = 0; s < nsteps; s += 3) {
+      GEMM_STEP(s, aA, aB, wA, 0)
+      GEMM_STEP(s + 1, aB, aC, wB, 1)
+      GEMM_STEP(s + 2, aC, aA, wC, 2)
+    }
   }
 #undef GEMM_STEP
 
@@ -198,10 +225,21 @@ __global__ void __launch_bounds__(256) k_gemm(GemmArgs g) {
 template <int MT>
 void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   dim3 grid(g.N / 128, splits, cdiv_i(g.M, MT * 16));
-  if (epi == EPI_PARTIAL)
-    k_gemm<MT, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
-  else
-    k_gemm<MT, EPI_ARGMAX><<<grid, 256, 0, st>>>(g);
+  const int steps = g.kper / KS;
+  const bool exact = (int64_t)g.kper * splits == g.K;
+  if (epi == EPI_ARGMAX) {
+    k_gemm<MT, 0, EPI_ARGMAX><<<grid, 256, 0, st>>>(g);
+  } else if (exact && steps == 4) {
+    k_gemm<MT, 4, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+  } else if (exact && steps == 8) {
+    k_gemm<MT, 8, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+  } else if (exact && steps == 12) {
+    k_gemm<MT, 12, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+  } else if (exact && steps == 16) {
+    k_gemm<MT, 16, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+  } else {
+    k_gemm<MT, 0, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+  }
 }
 
 }  // namespace

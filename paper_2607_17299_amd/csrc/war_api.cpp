@@ -215,16 +215,26 @@ struct Timed {
   }
 };
 
+// Split-K: the largest step count per split (16, 12, 8 or 4 steps of 64) that
+// divides K exactly and still gives >= 512 workgroups (2 per CU); the fully
+// unrolled kernels need exact splits.
 Split pick_split(int M, int N, int K, int64_t cap_elems) {
   const int mt = gemm_mt(M);
   const int mblocks = cdiv_i(M, mt * 16);
   const int base = (N / 128) * mblocks;
-  int s = std::max(1, (int)std::lround(1024.0 / base));
-  s = std::min(s, std::max(1, K / 512));
+  for (int steps : {16, 12, 8, 4}) {
+    const int kper = steps * 64;
+    if (K % kper) continue;
+    const int s = K / kper;
+    if ((int64_t)base * s >= 512 || steps == 4) {
+      if ((int64_t)s * M * N <= cap_elems) return {s, kper};
+    }
+  }
+  // fall back: one split per 1024 of K (runtime-loop kernel)
+  int s = std::max(1, K / 1024);
   while (s > 1 && (int64_t)s * M * N > cap_elems) --s;
-  int kper = cdiv_i(cdiv_i(K, s), 64) * 64;
-  s = cdiv_i(K, kper);
-  return {s, kper};
+  const int kper = cdiv_i(cdiv_i(K, s), 64) * 64;
+  return {cdiv_i(K, kper), kper};
 }
 
 // One projection: P[split][M][N] = A x W^T (or the LM-head argmax epilogue).
