@@ -66,7 +66,7 @@ typedef struct war_model_config {
   int32_t max_rows;  /* most rows one forward pass holds (verify: B*(k_max+1)) */
 } war_model_config;
 
-typedef struct war_model war_model;     /* opaque: borrowed weights + owned workspace */
+typedef struct war_model war_model;     /* opaque: owned weight copy + owned workspace */
 typedef struct war_kv_pool war_kv_pool; /* opaque: owned allocator state, borrowed KV */
 
 /* Number of weight pointers a model takes: 3 + 7 * n_layers. */
@@ -85,8 +85,12 @@ int32_t war_weight_count(const war_model_config* cfg);
  *     w_down [d, F];
  *   then final_norm [d];
  *   then w_lm [V, d].
- * The model borrows the pointers: they must outlive it.  It allocates its own
- * device workspace (sized by max_rows).  Returns WAR_ERR_UNSUPPORTED for shapes
+ * The model copies every weight into device memory it owns, the projection
+ * and LM-head matrices repacked into the order its GEMM kernel streams
+ * (16-row by 64-column MFMA fragments, each 16-byte lane chunk contiguous), so
+ * the caller's buffers are not read after this call returns and may be freed.
+ * The copy costs as much device memory as the weights themselves.  The model
+ * also allocates its own device workspace (sized by max_rows).  Returns WAR_ERR_UNSUPPORTED for shapes
  * outside the constraints above. */
 war_status war_model_create(const war_model_config* cfg, const void* const* weights,
                             int32_t n_weights, war_model** out);

@@ -5,11 +5,19 @@
 // against N x K weights of 16-310 MB, so the kernel is bound by streaming W
 // from HBM: every weight byte is read exactly once per m-block.
 //
+// Weights are repacked once, when the model is created, into MFMA fragment
+// order: for n-tile nt (16 output rows), k-step s (64 inputs) and half j, the
+// 1 KB fragment holds, for lane l, the 8 values
+//     W[nt*16 + l%16][s*64 + (l/16)*16 + j*8 + e],  e = 0..7,
+// and fragments are stored nt-major, then s, then j.  One wave-wide 16-byte
+// load then reads 1 KB of contiguous memory, and a wave walking k for one
+// n-tile streams a contiguous run (2 KB per step) -- the HBM-friendly pattern
+// of a plain copy, where row-major W would touch 16 rows 8-24 KB apart per load.
+//
 // Workgroup = 4 waves = 128 output columns; each wave owns 32 columns (two
 // 16-wide MFMA n-tiles) and all MT 16-row m-tiles of the workgroup's m-block.
 // K advances in steps of 64:
-//   * W goes straight from HBM to registers -- each lane reads 32 contiguous
-//     bytes of two W rows per step (4 lanes cover a 128-byte line);
+//   * W goes straight from HBM to registers (4 fragments per wave and step);
 //   * the A tile (MT*16 rows x 64) is loaded into registers by all 256 threads
 //     and staged through LDS (three buffers, rows padded to 144 bytes), shared
 //     by the 4 waves;
@@ -45,14 +53,31 @@ template <int MT, int NSTEPS, int EPI>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm(GemmArgs g) {
   __shared__ __attribute__((aligned(16))) unsigned char sA[3][Tile<MT>::BYTES];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
+  // Workgroups are dealt to the 8 XCDs round-robin by linear id.  The m-blocks
+  // of one weight block get ids 8 apart (same XCD, dispatched together), so
+  // all but the first find W in that XCD's L2; a ragged tail of fewer than 8
+  // n-blocks falls back to consecutive ids.
+  const int mblocks = (g.M + MT * 16 - 1) / (MT * 16);
+  const int NB = g.N / 128;
+  const int full = (NB / 8) * 8 * mblocks;
+  int nb, mb;
+  if ((int)blockIdx.x < full) {
+    const int r = blockIdx.x % (8 * mblocks);
+    nb = (blockIdx.x / (8 * mblocks)) * 8 + (r & 7);
+    mb = r >> 3;
+  } else {
+    const int r = blockIdx.x - full;
+    nb = (NB / 8) * 8 + r / mblocks;
+    mb = r % mblocks;
+  }
   const int split = blockIdx.y;
-  const int m0 = blockIdx.z * MT * 16;
+  const int m0 = mb * MT * 16;
   const int kb = split * g.kper;
   const int ke = min(g.K, kb + g.kper);
   const int nsteps = NSTEPS > 0 ? NSTEPS : (ke - kb) / KS;
-  const int n0 = blockIdx.x * 128;
-  const bf16_t* Wb = n0 < g.n_split ? g.W1 + (int64_t)n0 * g.ldw
-                                    : g.W2 + (int64_t)(n0 - g.n_split) * g.ldw;
+  const int n0 = nb * 128;
+  const int S = g.K / KS;  // k-steps per n-tile in the packed layout
+  const bf16_t* Wb = g.Wp + (int64_t)(n0 / 16) * S * (KS * 16);
 
   // Loads are raw buffer loads (one descriptor for the W block, one for A): the
   // compiler does not re-issue them next to their use, so they stay in flight
@@ -64,8 +89,9 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(Wb), 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t ares =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(g.A), 0, 0x7fffffff, 0x00020000);
-  const int wv0 = ((w * 32 + ln) * g.ldw + kb + lg * 16) * 2;  // byte offsets
-  const int wv1 = wv0 + 16 * g.ldw * 2;
+  // byte offsets of this lane's fragments of step 0 (n-tiles 2w and 2w+1)
+  const int wv0 = ((w * 2) * S + kb / KS) * (KS * 32) + lane * 16;
+  const int wv1 = wv0 + S * (KS * 32);
   int av[Tile<MT>::PER_THREAD];
   int aoff[Tile<MT>::PER_THREAD];
 #pragma unroll
@@ -82,10 +108,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
   };
   auto load_w = [&](uint4* wr, int s) {
-    wr[0] = bload(wres, wv0, s * KS * 2);
-    wr[1] = bload(wres, wv0 + 16, s * KS * 2);
-    wr[2] = bload(wres, wv1, s * KS * 2);
-    wr[3] = bload(wres, wv1 + 16, s * KS * 2);
+    wr[0] = bload(wres, wv0, s * KS * 32);
+    wr[1] = bload(wres, wv0 + 1024, s * KS * 32);
+    wr[2] = bload(wres, wv1, s * KS * 32);
+    wr[3] = bload(wres, wv1 + 1024, s * KS * 32);
   };
   auto load_a = [&](uint4* ar, int s) {
 #pragma unroll
@@ -216,15 +242,15 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
           idx = oi;
         }
       }
-      g.amax_v[(int64_t)m * gridDim.x + blockIdx.x] = v;
-      g.amax_i[(int64_t)m * gridDim.x + blockIdx.x] = idx;
+      g.amax_v[(int64_t)m * (g.N / 128) + nb] = v;
+      g.amax_i[(int64_t)m * (g.N / 128) + nb] = idx;
     }
   }
 }
 
 template <int MT>
 void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
-  dim3 grid(g.N / 128, splits, cdiv_i(g.M, MT * 16));
+  dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 16), splits, 1);
   const int steps = g.kper / KS;
   const bool exact = (int64_t)g.kper * splits == g.K;
   if (epi == EPI_ARGMAX) {
@@ -242,9 +268,37 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   }
 }
 
+// One 16-byte fragment chunk per thread: chunk c = ((nt * S + s) * 2 + j) * 64 + l.
+__global__ void k_pack_weights(const bf16_t* __restrict__ W, int K, int64_t chunks,
+                               uint4* __restrict__ dst) {
+  const int S = K / KS;
+  for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < chunks;
+       c += (int64_t)gridDim.x * blockDim.x) {
+    const int l = (int)(c & 63);
+    const int j = (int)((c >> 6) & 1);
+    const int64_t ts = c >> 7;  // nt * S + s
+    const int64_t nt = ts / S;
+    const int s = (int)(ts - nt * S);
+    const int64_t row = nt * 16 + (l & 15);
+    const int col = s * KS + (l >> 4) * 16 + j * 8;
+    dst[c] = *reinterpret_cast<const uint4*>(W + row * K + col);
+  }
+}
+
 }  // namespace
 
-int gemm_mt(int M) { return std::min(12, std::max(1, cdiv_i(M, 16))); }
+void launch_pack_weights(const bf16_t* W, int N, int K, bf16_t* dst, hipStream_t st) {
+  const int64_t chunks = (int64_t)N * K / 8;
+  const int blocks = (int)std::min<int64_t>((chunks + 255) / 256, 16384);
+  k_pack_weights<<<blocks, 256, 0, st>>>(W, K, chunks, reinterpret_cast<uint4*>(dst));
+}
+
+// 16-row tiles per workgroup: up to 6 (96 rows); more rows take more m-blocks
+int gemm_mt(int M) {
+  const int t = std::max(1, cdiv_i(M, 16));
+  if (t <= 6) return t;
+  return cdiv_i(t, cdiv_i(t, 6));  // balanced m-blocks of at most 6 tiles
+}
 
 void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   switch (gemm_mt(g.M)) {

@@ -34,9 +34,7 @@ struct GemmArgs {
   const bf16_t* A;
   int lda;
   const int32_t* a_rows;  // nullable: A row m -> a_rows[m]
-  const bf16_t* W1;
-  const bf16_t* W2;
-  int n_split, ldw;
+  const bf16_t* Wp;  // weights in MFMA fragment order (launch_pack_weights)
   int M, N, K, kper;
   float* P;  // partial sums [split][M][N]
   // argmax epilogue (split == 1): per (row, 128-column block) best value and index
@@ -81,6 +79,8 @@ void launch_add_ctx(int n, int32_t* ctx, const int32_t* add, hipStream_t st);
 // GEMM (gemm.hip)
 int gemm_mt(int M);  // 16-row tiles per workgroup for M rows
 void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st);
+// W [N][K] row-major -> dst in MFMA fragment order; N % 16 == 0, K % 64 == 0
+void launch_pack_weights(const bf16_t* W, int N, int K, bf16_t* dst, hipStream_t st);
 
 // attention (attn.hip)
 int attn_rows_per_block(int G, int k_rows);  // RB (16, 32 or 48)

@@ -61,8 +61,10 @@ struct DevBuf {
   }
 };
 
+// Pointers into the model's own weight copy; the matrices are in MFMA fragment
+// order (w_gate_up = gate rows then up rows, one N = 2F matrix).
 struct LayerW {
-  const bf16_t *attn_norm, *w_qkv, *w_o, *ffn_norm, *w_gate, *w_up, *w_down;
+  const bf16_t *attn_norm, *w_qkv, *w_o, *ffn_norm, *w_gate_up, *w_down;
 };
 
 constexpr int kMaxBatch = 1024;
@@ -96,6 +98,7 @@ struct war_model {
   std::vector<LayerW> layers;
   const bf16_t* final_norm;
   const bf16_t* w_lm;
+  DevBuf wts;  // owned copy of every weight (matrices packed)
   int max_rows;
   // workspace
   DevBuf h, u, q, o, P, cos_t, sin_t, inv_freq, amax_v, amax_i;
@@ -238,17 +241,14 @@ Split pick_split(int M, int N, int K, int64_t cap_elems) {
 }
 
 // One projection: P[split][M][N] = A x W^T (or the LM-head argmax epilogue).
-war_status gemm(war_model* m, const bf16_t* A, int lda, const int32_t* a_rows, const bf16_t* W1,
-                const bf16_t* W2, int n_split, int M, int N, int K, int* splits_out,
-                hipStream_t st, bool argmax = false, float* logits = nullptr) {
+war_status gemm(war_model* m, const bf16_t* A, int lda, const int32_t* a_rows, const bf16_t* Wp,
+                int M, int N, int K, int* splits_out, hipStream_t st, bool argmax = false,
+                float* logits = nullptr) {
   GemmArgs g{};
   g.A = A;
   g.lda = lda;
   g.a_rows = a_rows;
-  g.W1 = W1;
-  g.W2 = W2 ? W2 : W1;
-  g.n_split = W2 ? n_split : N;
-  g.ldw = K;
+  g.Wp = Wp;
   g.M = M;
   g.N = N;
   g.K = K;
@@ -291,7 +291,7 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
     int s = 1;
     {
       Timed t(pf, st, "gemm_qkv");
-      gemm(m, u, md.d, nullptr, L.w_qkv, nullptr, 0, R, md.qkv, md.d, &s, st);
+      gemm(m, u, md.d, nullptr, L.w_qkv, R, md.qkv, md.d, &s, st);
     }
     {
       Timed t(pf, st, "qkv_rope_kvwrite");
@@ -310,7 +310,7 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
     }
     {
       Timed t(pf, st, "gemm_o");
-      gemm(m, o, md.nq * md.hd, nullptr, L.w_o, nullptr, 0, R, md.d, md.nq * md.hd, &s, st);
+      gemm(m, o, md.nq * md.hd, nullptr, L.w_o, R, md.d, md.nq * md.hd, &s, st);
     }
     {
       Timed t(pf, st, "residual_norm");
@@ -318,7 +318,7 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
     }
     {
       Timed t(pf, st, "gemm_gate_up");
-      gemm(m, u, md.d, nullptr, L.w_gate, L.w_up, md.F, R, 2 * md.F, md.d, &s, st);
+      gemm(m, u, md.d, nullptr, L.w_gate_up, R, 2 * md.F, md.d, &s, st);
     }
     {
       Timed t(pf, st, "swiglu");
@@ -326,7 +326,7 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
     }
     {
       Timed t(pf, st, "gemm_down");
-      gemm(m, u, md.F, nullptr, L.w_down, nullptr, 0, R, md.d, md.F, &s, st);
+      gemm(m, u, md.F, nullptr, L.w_down, R, md.d, md.F, &s, st);
     }
     const bf16_t* gnext = l + 1 < m->cfg.n_layers ? m->layers[l + 1].attn_norm : m->final_norm;
     {
@@ -426,22 +426,53 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
   md.V = cfg->vocab;
   md.qkv = (md.nq + 2 * md.nkv) * md.hd;
   md.eps = cfg->rms_eps;
+  // One owned allocation: embedding (row-major), norm gains, and every matrix
+  // repacked into MFMA fragment order.  The caller's buffers are read here
+  // (stream-ordered on the null stream, then synchronised) and never again.
+  const int64_t d = md.d, F = md.F, V = md.V, nqhd = (int64_t)md.nq * md.hd;
+  const int64_t per_layer = 2 * d + (int64_t)md.qkv * d + d * nqhd + 2 * F * d + d * F;
+  const int64_t total = 2 * V * d + d + cfg->n_layers * per_layer;
+  if (hipError_t e0 = m->wts.ensure((size_t)total * 2); e0 != hipSuccess) {
+    delete m;
+    return fail(WAR_ERR_HIP, std::string("weight allocation: ") + hipGetErrorString(e0));
+  }
+  bf16_t* dst = m->wts.as<bf16_t>();
   int k = 0;
-  auto W = [&]() { return static_cast<const bf16_t*>(weights[k++]); };
-  m->embed = W();
+  auto src = [&]() { return static_cast<const bf16_t*>(weights[k++]); };
+  hipError_t ecopy = hipSuccess;
+  auto copy = [&](int64_t n) {
+    bf16_t* at = dst;
+    const hipError_t ec = hipMemcpyAsync(at, src(), (size_t)n * 2, hipMemcpyDeviceToDevice, nullptr);
+    if (ecopy == hipSuccess) ecopy = ec;
+    dst += n;
+    return at;
+  };
+  auto pack = [&](int64_t N, int64_t K) {
+    bf16_t* at = dst;
+    launch_pack_weights(src(), (int)N, (int)K, at, nullptr);
+    dst += N * K;
+    return at;
+  };
+  m->embed = copy(V * d);
   for (int l = 0; l < cfg->n_layers; ++l) {
     LayerW L;
-    L.attn_norm = W();
-    L.w_qkv = W();
-    L.w_o = W();
-    L.ffn_norm = W();
-    L.w_gate = W();
-    L.w_up = W();
-    L.w_down = W();
+    L.attn_norm = copy(d);
+    L.w_qkv = pack(md.qkv, d);
+    L.w_o = pack(d, nqhd);
+    L.ffn_norm = copy(d);
+    L.w_gate_up = pack(F, d);  // gate rows, then
+    pack(F, d);                // up rows directly after them
+    L.w_down = pack(d, F);
     m->layers.push_back(L);
   }
-  m->final_norm = W();
-  m->w_lm = W();
+  m->final_norm = copy(d);
+  m->w_lm = pack(V, d);
+  if (ecopy == hipSuccess) ecopy = hipGetLastError();
+  if (hipError_t e0 = hipDeviceSynchronize(); e0 != hipSuccess || ecopy != hipSuccess) {
+    if (e0 == hipSuccess) e0 = ecopy;
+    war_model_destroy(m);
+    return fail(WAR_ERR_HIP, std::string("weight copy: ") + hipGetErrorString(e0));
+  }
   const int R = cfg->max_rows;
   m->max_rows = R;
   m->n_req_cap = std::max(R, kMaxBatch);
@@ -480,7 +511,7 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
 
 void war_model_destroy(war_model* m) {
   if (!m) return;
-  for (DevBuf* b : {&m->h, &m->u, &m->q, &m->o, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
+  for (DevBuf* b : {&m->wts, &m->h, &m->u, &m->q, &m->o, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
                     &m->amax_v, &m->amax_i, &m->rows_i32, &m->reqs_i32, &m->segs_i32, &m->n_items,
                     &m->items, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
     b->release();
@@ -725,7 +756,7 @@ war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_
   int sdummy;
   {
     Timed t(m->prof, st, "gemm_lm_head_argmax");
-    gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, nullptr, 0, R, m->md.V, m->md.d, &sdummy,
+    gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, R, m->md.V, m->md.d, &sdummy,
          st, true, logits);
   }
   {
@@ -889,7 +920,7 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
       const int nl = (int)last_rows.size();
       HIPCHK(hipMemcpyAsync(m->a_rows.p, last_rows.data(), nl * 4, hipMemcpyHostToDevice, st));
       int sd;
-      gemm(m, m->u.as<bf16_t>(), m->md.d, m->a_rows.as<int32_t>(), m->w_lm, nullptr, 0, nl, m->md.V,
+      gemm(m, m->u.as<bf16_t>(), m->md.d, m->a_rows.as<int32_t>(), m->w_lm, nl, m->md.V,
            m->md.d, &sd, st, true, last_logits ? last_logits + (int64_t)first_seq * m->md.V : nullptr);
       launch_argmax_accept(nl, nullptr, 1, m->md.V / 128, m->amax_v.as<float>(), m->amax_i.as<int32_t>(),
                            nullptr, 0, nullptr, next_tokens + first_seq, st);

@@ -109,18 +109,20 @@ def config_struct(cfg: ModelConfig, max_rows: int) -> _Config:
 
 
 class Model:
-    """A decoder over caller-owned bf16 device weights (canonical order)."""
+    """A decoder over bf16 device weights (canonical order).  The library copies
+    (and repacks) them at creation; the tensors may be dropped afterwards."""
 
     def __init__(self, cfg: ModelConfig, weights: Dict[str, torch.Tensor], max_rows: int = 1024):
         self.cfg, self.max_rows = cfg, max_rows
         names = [n for n, _ in weight_shapes(cfg)]
-        self._w = [weights[n] for n in names]      # keeps the borrowed tensors alive
-        for t in self._w:
+        ws = [weights[n] for n in names]
+        for t in ws:
             assert t.is_cuda and t.dtype == torch.bfloat16 and t.is_contiguous()
-        arr = (C.c_void_p * len(self._w))(*[t.data_ptr() for t in self._w])
+        arr = (C.c_void_p * len(ws))(*[t.data_ptr() for t in ws])
         self._cfg = config_struct(cfg, max_rows)
         h = C.c_void_p()
-        _check(lib().war_model_create(C.byref(self._cfg), arr, len(self._w), C.byref(h)))
+        torch.cuda.synchronize()                    # the weights are complete before the copy
+        _check(lib().war_model_create(C.byref(self._cfg), arr, len(ws), C.byref(h)))
         self.handle = h
 
     def close(self):
