@@ -1,13 +1,17 @@
 #!/usr/bin/env python3
 """Benchmark of the speculative-verification decode step on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload low_load|high_load|high_load_k2]
+    python bench.py [--steps K] [--warmup W] [--workload low_load|high_load|high_load_k2|multi_turn]
 
 A step is one pass of the whole hot path over one batch: war_verify_step (page
 reservation, embedding, 36 decoder layers with paged GQA verification attention,
 LM head, argmax and greedy acceptance) followed by war_kv_commit.  Each timed step
 discards (accept = -1, the rollback path), so that every step starts from the
 same state.  Inputs are resident in HBM before timing starts.
+
+multi_turn first appends a 2048-token observation to each of 16 cached
+trajectories with war_prefill_append (timed once, reported under "prefill"),
+then times the k = 4 verify step that follows.
 
 Prints ONE JSON line:
   value     accepted tokens/s = sum_b (accept_b + 1) / step time;
@@ -36,7 +40,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="low_load",
-                    choices=["low_load", "high_load", "high_load_k2"])
+                    choices=["low_load", "high_load", "high_load_k2", "multi_turn"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--copy-probe", action="store_true",
@@ -122,6 +126,28 @@ def cpu_baseline(cfg, weights, st, kv_seed, sample_layers: int = 8):
             "sample_layers": sample_layers}
 
 
+def time_prefill(model, pool, mt, cfg):
+    """One war_prefill_append over the multi-turn workload, timed with events."""
+    import torch
+    from paper_2607_17299_amd import harness
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    nxt, _, _ = harness.multi_turn_append(model, pool, mt)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    d, L, nq, hd = cfg.d_model, cfg.n_layers, cfg.n_q_heads, cfg.head_dim
+    layer_params = d * (nq + 2 * cfg.n_kv_heads) * hd + nq * hd * d + 3 * d * cfg.ffn_dim
+    n_tok = mt.n * mt.n_new
+    # token at position p attends p + 1 keys: QK^T and PV, 2 flops per multiply-add
+    keys = mt.n * sum(mt.cached + i + 1 for i in range(mt.n_new))
+    flops = 2 * n_tok * L * layer_params + 2 * mt.n * cfg.vocab * d + 4 * L * nq * hd * keys
+    return {"ms": round(ms, 2), "tokens": n_tok, "tokens_per_s": round(n_tok / (ms / 1e3), 1),
+            "flops": flops, "achieved_TFLOPs": round(flops / (ms / 1e3) / 1e12, 1),
+            "peak_TFLOPs": 2500.0, "next_tokens": nxt.cpu().numpy()}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -155,19 +181,32 @@ def main():
     weights = harness.large_weights(cfg)
     model = war.Model(cfg, weights, max_rows=1024)
     kv_seed = 5
+    prefill = None
     if args.workload == "low_load":
         st = harness.low_load_step()
         desc = ("low-load rollout verify: 36-layer GQA decoder (d 4096, 32q/8kv heads, hd 128, FFN 12288, "
                 "vocab 151936), 8 requests x 32768 cached tokens, k=8 suffix-drafter drafts")
+    elif args.workload == "multi_turn":
+        mt = harness.multi_turn_inputs(vocab=cfg.vocab)
+        desc = ("multi-turn append: 36-layer GQA decoder, 16 trajectories in 4 groups sharing a forked "
+                "8192-token prefix, 24576 cached tokens each; war_prefill_append of a 2048-token "
+                "observation each, then one k=4 verify step (suffix drafts over the group's siblings)")
+        pool = harness.multi_turn_pool(cfg, mt, 4)
+        log("loading cached prefixes (forked) and private contexts")
+        harness.load_multi_turn(pool, cfg, mt, kv_seed)
+        log("prefill-append")
+        prefill = time_prefill(model, pool, mt, cfg)
+        st = harness.multi_turn_step(mt, prefill.pop("next_tokens"), 4)
     else:
         k = 2 if args.workload == "high_load_k2" else 0
         st = harness.high_load_step(k=0)
         desc = ("high-load rollout %s: 36-layer GQA decoder, 64 requests, lognormal contexts "
                 "(median 8192, sigma 0.8, seed 0)" % ("verify k=2 (sibling drafts, 30%% corrupted)" if k else "decode k=0"))
     log(f"workload {args.workload}: B={st.B} k={st.k_max} sum ctx={int(st.ctx_lens.sum())}")
-    pool = harness.make_pool(cfg, st.ctx_lens, max(st.k_max, 2) + 8)
-    log("loading cached contexts")
-    harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, kv_seed)
+    if args.workload != "multi_turn":
+        pool = harness.make_pool(cfg, st.ctx_lens, max(st.k_max, 2) + 8)
+        log("loading cached contexts")
+        harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, kv_seed)
     if args.workload == "high_load_k2":
         cont = harness.teacher_continuation(model, pool, st, 2)
         drafts = harness.corrupt(cont, 0.3, seed=4, vocab=cfg.vocab)
@@ -194,11 +233,12 @@ def main():
     traffic = measured_traffic(args.workload)
 
     variants = {}
-    if args.workload == "low_load" and not args.no_variants:
+    if args.workload in ("low_load", "multi_turn") and not args.no_variants:
         # the same requests, drafting from a sibling rollout that produced the
         # target's own continuation (GRPO siblings): drafts are accepted
         cont = harness.teacher_continuation(model, pool, st, st.k_max + 1)
-        st2 = harness.low_load_step(siblings=cont)
+        st2 = (harness.low_load_step(siblings=cont) if args.workload == "low_load"
+               else harness.multi_turn_step(mt, st.last_tokens, st.k_max, siblings=cont))
         ds2 = harness.DeviceStep(st2)
         for _ in range(2):
             ds2.verify(model, pool)
@@ -237,6 +277,7 @@ def main():
                      "bytes_per_launch": kv_bytes, "mean_launch_ms": round(per_launch_ms, 5),
                      "traffic": traffic},
         "kernels_ms_per_step": prof,
+        "prefill": prefill,
         "variants": variants,
         "cpu_baseline": cpu,
     }

@@ -174,6 +174,111 @@ def corrupt(drafts: List[List[int]], p: float, seed: int, vocab: int) -> List[Li
     return out
 
 
+@dataclasses.dataclass
+class MultiTurn:
+    """Multi-turn append workload: ``groups`` x ``per_group`` trajectories.  The
+    trajectories of a group share a ``prefix``-token cached prefix (forked
+    pages), each has ``private`` more cached tokens of its own, and receives an
+    ``n_new``-token observation (uniform random ids) through war_prefill_append
+    (System Design, "Overview of WAR": a new turn appended to a cached
+    trajectory; GRPO siblings share their prompt)."""
+    groups: int
+    per_group: int
+    prefix: int
+    private: int
+    n_new: int
+    obs: List[np.ndarray]
+
+    @property
+    def n(self) -> int:
+        return self.groups * self.per_group
+
+    @property
+    def seq_ids(self) -> np.ndarray:
+        return np.arange(self.n, dtype=np.int32)
+
+    @property
+    def cached(self) -> int:
+        return self.prefix + self.private
+
+    def kv_parts(self, s: int):
+        """(generator key, first position, length) of trajectory s's cached context."""
+        return [(PREFIX_KEY + s // self.per_group, 0, self.prefix), (s, self.prefix, self.private)]
+
+
+PREFIX_KEY = 100000
+
+
+def multi_turn_inputs(seed: int = 5, groups: int = 4, per_group: int = 4, prefix: int = 8192,
+                      private: int = 16384, n_new: int = 2048, vocab: int = 151936) -> MultiTurn:
+    obs = [synth.uniform_tokens(seed * 1000 + s, n_new, vocab) for s in range(groups * per_group)]
+    return MultiTurn(groups, per_group, prefix, private, n_new, obs)
+
+
+def multi_turn_pool(cfg: synth.ModelConfig, mt: MultiTurn, k_max: int, extra_pages: int = 64) -> war.Pool:
+    P = cfg.page_size
+    assert mt.prefix % P == 0, "shared prefixes are whole pages"
+    own = cdiv(mt.cached + mt.n_new + k_max + 1, P) - mt.prefix // P
+    need = mt.groups * (mt.prefix // P) + mt.n * own + extra_pages
+    return war.Pool(cfg, need, mt.n, cdiv(mt.cached + mt.n_new + max(k_max, 64) + 1, P))
+
+
+def load_multi_turn(pool: war.Pool, cfg: synth.ModelConfig, mt: MultiTurn, kv_seed: int) -> None:
+    """Each group's prefix is loaded once and forked to its siblings; then every
+    trajectory gets its private cached tokens."""
+    for g in range(mt.groups):
+        s0 = g * mt.per_group
+        pool.alloc([s0], [mt.prefix])
+        for l in range(cfg.n_layers):
+            pool.load(s0, l, 0, synth.kv_context(cfg, kv_seed, PREFIX_KEY + g, l, 0, mt.prefix, "cuda"))
+        for j in range(1, mt.per_group):
+            pool.fork(s0, s0 + j, mt.prefix)
+    pool.alloc([int(s) for s in mt.seq_ids], [mt.cached] * mt.n)
+    for s in range(mt.n):
+        for l in range(cfg.n_layers):
+            pool.load(s, l, mt.prefix, synth.kv_context(cfg, kv_seed, s, l, mt.prefix, mt.private, "cuda"))
+    torch.cuda.synchronize()
+
+
+def multi_turn_kv(cfg: synth.ModelConfig, mt: MultiTurn, kv_seed: int, s: int, layer: int,
+                  device="cuda") -> torch.Tensor:
+    """[2, Hkv, cached, D] cached keys/values of trajectory s (what the pool holds)."""
+    return torch.cat([synth.kv_context(cfg, kv_seed, key, layer, p0, n, device)
+                      for key, p0, n in mt.kv_parts(s)], dim=2)
+
+
+def multi_turn_append(model: war.Model, pool: war.Pool, mt: MultiTurn, last_logits: bool = False):
+    """war_prefill_append of every trajectory's observation; returns (next
+    tokens, device ctx_lens, last-row logits or None)."""
+    t = lambda a: torch.as_tensor(np.asarray(a), dtype=torch.int32).cuda()
+    ctx = t(np.full(mt.n, mt.cached, np.int32))
+    nxt = t(np.zeros(mt.n, np.int32))
+    logits = torch.zeros((mt.n, model.cfg.vocab), device="cuda") if last_logits else None
+    war.prefill_append(model, pool, t(mt.seq_ids), ctx, [mt.n_new] * mt.n, t(np.concatenate(mt.obs)),
+                       nxt, logits)
+    return nxt, ctx, logits
+
+
+def multi_turn_step(mt: MultiTurn, next_tokens, k: int = 4,
+                    siblings: Optional[List[List[int]]] = None) -> Step:
+    """The verify step after the append.  Drafts come from the suffix drafter
+    over the other trajectories of the same group (their observations, and, when
+    given, a sibling rollout that produced each trajectory's continuation)."""
+    nxt = np.asarray(next_tokens, np.int32)
+    drafts = []
+    for s in range(mt.n):
+        d = SuffixDrafter()
+        g0 = (s // mt.per_group) * mt.per_group
+        for j in range(g0, g0 + mt.per_group):
+            if j != s:
+                d.add_trajectory(mt.obs[j])
+        ctx_tokens = np.concatenate([mt.obs[s], nxt[s:s + 1]])
+        if siblings is not None:
+            d.add_trajectory(np.concatenate([ctx_tokens[-64:], siblings[s]]))
+        drafts.append(d.propose(ctx_tokens, k))
+    return Step(mt.seq_ids, np.full(mt.n, mt.cached + mt.n_new, np.int32), nxt, drafts, k)
+
+
 def step_kv_bytes(cfg: synth.ModelConfig, st: Step) -> int:
     """KV bytes one layer's attention must read: every visible key and value."""
     per_tok = 2 * cfg.n_kv_heads * cfg.head_dim * 2

@@ -6,6 +6,8 @@ head_dim 128, FFN 12288, vocab 151936).
   tilings (k = 0, 2, 4, 8), contexts that are not multiples of a page or of
   an attention chunk, and the multi-chunk split-KV path.
 * Prefill-append on the same shapes, then a verify step on the appended KV.
+* The multi-turn append path: forked shared prefixes, an appended observation,
+  then a k = 4 verify step.
 * The full 36-layer low-load workload exactly as the benchmark runs it (8 x
   32768 cached tokens, k = 8), checked on a sampled request.
 The cached contexts come from the seeded generator (an input of the step), so
@@ -16,7 +18,7 @@ import pytest
 import torch
 
 from oracle.decoder import RequestKV, Weights, forward_block
-from oracle.verify import prefill_request, verify_request
+from oracle.verify import greedy_decode, prefill_request, verify_request
 from paper_2607_17299_amd import harness, synth
 from parity import compare_request, fp32_drift_tol
 
@@ -148,6 +150,72 @@ def test_reduced_depth_prefill_append(large2):
         K, V = kv.get(1)
         np.testing.assert_allclose(g[0][:, ctxs[b]:], K[:, ctxs[b]:], atol=3e-2, rtol=2e-2)
         np.testing.assert_allclose(g[1][:, ctxs[b]:], V[:, ctxs[b]:], atol=3e-2, rtol=2e-2)
+
+
+def test_reduced_depth_multi_turn(large2):
+    """The multi-turn append path on the full widths at 2 layers: 2 groups x 2
+    trajectories whose cached contexts share a forked 256-token prefix plus
+    200 private tokens (456 cached: not a page multiple), a 300-token
+    observation appended to each (prefill chunks span the 512-row workspace),
+    then one k = 4 verify step.  Trajectory 0 drafts the oracle's own greedy
+    continuation (all accepted), trajectory 1 the same with its second draft
+    replaced (one accepted), the others draft from the suffix drafter."""
+    war, cfg, model, W = large2["war"], large2["cfg"], large2["model"], large2["W"]
+    mt = harness.multi_turn_inputs(seed=11, groups=2, per_group=2, prefix=256, private=200,
+                                   n_new=300, vocab=cfg.vocab)
+    pool = harness.multi_turn_pool(cfg, mt, 4)
+    harness.load_multi_turn(pool, cfg, mt, KV_SEED)
+    bt = pool.block_tables.cpu().numpy()
+    np.testing.assert_array_equal(bt[0, :16], bt[1, :16])        # the prefix pages are shared
+    np.testing.assert_array_equal(bt[2, :16], bt[3, :16])
+    assert len(set(bt[0, 16:29]) & set(bt[1, 16:29])) == 0        # the private ones are not
+    nxt, ctx_d, last = harness.multi_turn_append(model, pool, mt, last_logits=True)
+    torch.cuda.synchronize()
+    assert ctx_d.cpu().tolist() == [mt.cached + mt.n_new] * mt.n
+    gl, gnext = last.cpu().numpy(), nxt.cpu().numpy()
+    kvs, conts, onext = [], [], []
+    for s in range(mt.n):
+        full = [harness.multi_turn_kv(cfg, mt, KV_SEED, s, l).cpu().double().numpy() for l in range(cfg.n_layers)]
+        kv = RequestKV(cfg, [(a[0], a[1]) for a in full])
+        hf, new_kv = forward_block(cfg, W, [int(t) for t in mt.obs[s]], kv.length, kv.get, want_logits=False)
+        kv.append(new_kv, mt.n_new)
+        z = hf[-1] @ W.get("w_lm").T
+        err = np.abs(gl[s] - z).max()
+        assert err < 5e-2, (s, err)
+        g = int(np.argmax(z))
+        if int(gnext[s]) != g:
+            zs = np.sort(z)
+            assert zs[-1] - zs[-2] <= 2 * err, (s, gnext[s], g)
+        # the appended keys/values in the pages match the oracle's
+        got = pool.gather_kv(s, mt.cached + mt.n_new, cfg.n_layers - 1).double().cpu().numpy()
+        K, V = kv.get(cfg.n_layers - 1)
+        np.testing.assert_allclose(got[0][:, mt.cached:], K[:, mt.cached:], atol=3e-2, rtol=2e-2)
+        np.testing.assert_allclose(got[1][:, mt.cached:], V[:, mt.cached:], atol=3e-2, rtol=2e-2)
+        np.testing.assert_array_equal(got[0][:, :mt.cached], full[-1][0])   # cached part untouched
+        kvs.append(kv)
+        onext.append(g)
+        conts.append(greedy_decode(cfg, W, RequestKV(cfg, list(kv.layers)), g, 4))
+    # the verify step's pending tokens are the oracle's argmax after the append
+    onext = np.array(onext, np.int32)
+    base = harness.multi_turn_step(mt, onext, 4)
+    drafts = [conts[0], [conts[1][0], (conts[1][1] + 1) % cfg.vocab] + conts[1][2:]] + base.drafts[2:]
+    st = harness.Step(mt.seq_ids, base.ctx_lens, onext, drafts, 4)
+    ds = harness.DeviceStep(st, with_logits=True, vocab=cfg.vocab)
+    ds.verify(model, pool, logits=True)
+    ds.commit(pool, discard=False)
+    torch.cuda.synchronize()
+    glog = ds.logits.cpu().numpy().reshape(st.B, 5, cfg.vocab)
+    acc, nx = ds.accept.cpu().numpy(), ds.next.cpu().numpy()
+    report, o_acc = [], []
+    for s in range(mt.n):
+        r = verify_request(cfg, W, kvs[s], int(onext[s]), st.drafts[s])
+        compare_request(r["logits"], glog[s], st.drafts[s], r["accept"], r["next"], int(acc[s]), int(nx[s]),
+                        report, f"multi_turn traj {s}")
+        o_acc.append(r["accept"])
+    # losslessness on the oracle side: its own continuation is accepted in full
+    assert o_acc[0] == 4 and o_acc[1] == 1, o_acc
+    np.testing.assert_array_equal(ds.ctx.cpu().numpy(), st.ctx_lens + acc + 1)
+    print(f"\nmulti_turn: accept {acc.tolist()}; {report}")
 
 
 def _oracle_kv_stream(cfg, kv_seed, seq, ctx, tag):
