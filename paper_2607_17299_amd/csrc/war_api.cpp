@@ -219,8 +219,10 @@ struct Timed {
 };
 
 // Split-K: the largest step count per split (16, 12, 8 or 4 steps of 64) that
-// divides K exactly and still gives >= 512 workgroups (2 per CU); the fully
-// unrolled kernels need exact splits.
+// divides K exactly and still gives >= 192 workgroups; the fully unrolled
+// kernels need exact splits.  Fewer splits mean fewer fp32 partial sums to
+// write and to add up afterwards; below ~192 workgroups too few CUs stream W
+// (measured on the 4096- and 6144-wide projections: 192-256 is the optimum).
 Split pick_split(int M, int N, int K, int64_t cap_elems) {
   const int mt = gemm_mt(M);
   const int mblocks = cdiv_i(M, mt * 16);
@@ -229,7 +231,7 @@ Split pick_split(int M, int N, int K, int64_t cap_elems) {
     const int kper = steps * 64;
     if (K % kper) continue;
     const int s = K / kper;
-    if ((int64_t)base * s >= 512 || steps == 4) {
+    if ((int64_t)base * s >= 192 || steps == 4) {
       if ((int64_t)s * M * N <= cap_elems) return {s, kper};
     }
   }
