@@ -43,6 +43,8 @@ def parse():
                     choices=["low_load", "high_load", "high_load_k2", "multi_turn"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only the speculation on/off sweep: step time over batch size x draft length")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only time a plain 2 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -126,6 +128,48 @@ def cpu_baseline(cfg, weights, st, kv_seed, sample_layers: int = 8):
             "sample_layers": sample_layers}
 
 
+def run_sweep(model, cfg, kv_seed, steps, warmup):
+    """Verify-step time over batch size B x draft length k on fixed 8192-token
+    contexts (the paper's batch sweep fixes the input at 8192 tokens), and the
+    draft length the speculation policy picks from it."""
+    import numpy as np
+    from paper_2607_17299_amd import harness, policy, synth
+    batches, ks, ctx = [1, 2, 4, 8, 16, 32, 64, 128], [0, 2, 4, 8], 8192
+    seq = np.arange(max(batches), dtype=np.int32)
+    ctxs = np.full(len(seq), ctx, np.int32)
+    pool = harness.make_pool(cfg, ctxs, max(ks))
+    log(f"loading {len(seq)} x {ctx} cached tokens")
+    harness.load_contexts(pool, cfg, ctxs, seq, kv_seed)
+    last = synth.uniform_tokens(91, len(seq), cfg.vocab)
+    table = {}
+    for B in batches:
+        for k in ks:
+            drafts = [[int(t) for t in synth.uniform_tokens(100000 + 1000 * B + 10 * k + b, k, cfg.vocab)]
+                      for b in range(B)]
+            ds = harness.DeviceStep(harness.Step(seq[:B], ctxs[:B], last[:B], drafts, k))
+            for _ in range(warmup):
+                ds.verify(model, pool)
+                ds.commit(pool, discard=True)
+            table[(B, k)] = timed_steps(ds, model, pool, steps)
+            log(f"B={B} k={k}: {table[(B, k)]:.3f} ms")
+    pol = policy.SpecPolicy(table)
+    alphas = [0.1, 0.2, 0.3, 0.5, 0.7, 0.9]
+    return {
+        "metric": "verify step time over batch size and draft length (speculation on/off sweep)",
+        "unit": "ms per step", "n_gpus": 1, "steps": steps, "warmup": warmup, "dtype": "bf16",
+        "data": "synthetic (seeded random-init weights, seeded cached KV, random drafts)",
+        "config": {"workload": "36-layer GQA decoder, B requests x 8192 cached tokens, k drafts each "
+                               "(timed with discard; the acceptance model is applied afterwards)",
+                   "batches": batches, "ks": ks},
+        "step_ms": {f"B={b}": {f"k={k}": round(table[(b, k)], 4) for k in ks} for b in batches},
+        "acceptance_model": "each draft accepted with probability alpha; E[tokens/step] = sum_j<=k alpha^j",
+        "tokens_per_s": {f"alpha={a}": {f"B={b}": {f"k={k}": round(pol.throughput(b, k, a), 1) for k in ks}
+                                        for b in batches} for a in alphas},
+        "chosen_k": {f"alpha={a}": {f"B={b}": pol.choose_k(b, a) for b in batches} for a in alphas},
+        "crossover_batch": {f"alpha={a}": pol.crossover(a) for a in alphas},
+    }
+
+
 def time_prefill(model, pool, mt, cfg):
     """One war_prefill_append over the multi-turn workload, timed with events."""
     import torch
@@ -179,8 +223,11 @@ def main():
     t_setup = time.perf_counter()
     log("generating weights on the GPU")
     weights = harness.large_weights(cfg)
-    model = war.Model(cfg, weights, max_rows=1024)
+    model = war.Model(cfg, weights, max_rows=1152 if args.sweep else 1024)
     kv_seed = 5
+    if args.sweep:
+        print(json.dumps(run_sweep(model, cfg, kv_seed, min(args.steps, 10), args.warmup)), flush=True)
+        return
     prefill = None
     if args.workload == "low_load":
         st = harness.low_load_step()
