@@ -260,6 +260,51 @@ def _run_steps(tiny, steps, draft_mode, seed, report):
     return stats
 
 
+def test_mode_switching_is_stateless(tiny):
+    """Consecutive steps with k_max = 0 (plain decode) and k_max > 0 on the same
+    pool and sequences (the speculation on/off switch): with the oracle's own
+    continuation as drafts every step accepts all of them, and the tokens
+    emitted over the whole schedule are the oracle's token-by-token greedy
+    stream."""
+    war, model, W = tiny["war"], tiny["model"], tiny["W"]
+    _, ctxs = _tiny_workload(seed=7, B=3, ctx_len=200)
+    pool, seq, ctx, kvs, onext, *_ = _prefill_both(tiny, ctxs)
+    start = [RequestKV(CFG, list(kv.layers)) for kv in kvs]
+    pending = [int(x) for x in onext]
+    emitted = [[] for _ in ctxs]
+    report = []
+    t = lambda a: torch.tensor(np.asarray(a), dtype=torch.int32, device=DEV)
+    for step, k in enumerate([0, 4, 0, 2, 8, 0, 1]):
+        drafts = [greedy_decode(CFG, W, copy.deepcopy(kvs[b]), pending[b], k) for b in range(len(ctxs))]
+        dt = np.zeros((len(ctxs), max(k, 1)), np.int32)
+        for b, d in enumerate(drafts):
+            dt[b, :k] = d
+        acc, nxt = t([0] * len(ctxs)), t([0] * len(ctxs))
+        logits = torch.zeros((len(ctxs) * (k + 1), CFG.vocab), device=DEV)
+        war.verify_step(model, pool, seq, ctx, t(pending), t(dt), t([k] * len(ctxs)), k, acc, nxt, logits)
+        war.kv_commit(pool, seq, ctx, acc)
+        torch.cuda.synchronize()
+        g_acc, g_nxt = acc.cpu().numpy(), nxt.cpu().numpy()
+        glog = logits.cpu().numpy().reshape(len(ctxs), k + 1, CFG.vocab)
+        for b in range(len(ctxs)):
+            r = verify_request(CFG, W, kvs[b], pending[b], drafts[b])
+            assert r["accept"] == k                      # the oracle accepts its own continuation
+            compare_request(r["logits"], glog[b], drafts[b], r["accept"], r["next"], int(g_acc[b]),
+                            int(g_nxt[b]), report, f"step {step} (k={k}) req {b}")
+            commit_request(kvs[b], r)
+            emitted[b] += drafts[b] + [r["next"]]
+            pending[b] = r["next"]
+        assert not report, report
+        assert ctx.cpu().tolist() == [kv.length for kv in kvs]
+    for b in range(len(ctxs)):
+        want = greedy_decode(CFG, W, start[b], int(onext[b]), len(emitted[b]))
+        assert emitted[b] == want
+        g = pool.gather_kv(b, kvs[b].length, CFG.n_layers - 1).double().cpu().numpy()
+        K, V = kvs[b].get(CFG.n_layers - 1)
+        np.testing.assert_allclose(g[0], K, atol=2e-2, rtol=2e-2)
+        np.testing.assert_allclose(g[1], V, atol=2e-2, rtol=2e-2)
+
+
 @pytest.mark.parametrize("mode", ["suffix", "greedy", "mixed"])
 def test_verify_steps_match_oracle(tiny, mode):
     report = []
