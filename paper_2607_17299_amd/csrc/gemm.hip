@@ -30,7 +30,10 @@
 // Split-K over blockIdx.y fills the 256 CUs when N is small; partial sums go to
 // P[split][M][N] and a row kernel adds them in a fixed order (deterministic).
 // The argmax epilogue (LM head, one split) writes optional fp32 logits and the
-// best (value, lowest index) of each row within each 128-column block.
+// best (value, lowest index) of each row within each 128-column block.  The
+// SwiGLU epilogue (gate/up, one split) takes the [gate; up] matrix with wave w
+// of block nb owning gate n-tile 4nb + w and the matching up n-tile, and
+// writes bf16 silu(gate) * up for its 16 columns.
 #include "kernels.h"
 
 namespace {
@@ -77,7 +80,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
   const int nsteps = NSTEPS > 0 ? NSTEPS : (ke - kb) / KS;
   const int n0 = nb * 128;
   const int S = g.K / KS;  // k-steps per n-tile in the packed layout
-  const bf16_t* Wb = g.Wp + (int64_t)(n0 / 16) * S * (KS * 16);
+  // first n-tile of the block: 8 consecutive tiles, or (SwiGLU) 4 gate tiles
+  // whose up tiles sit N/32 tiles further on
+  const int tb = EPI == EPI_SWIGLU ? nb * 4 : nb * 8;
+  const bf16_t* Wb = g.Wp + (int64_t)tb * S * (KS * 16);
 
   // Loads are raw buffer loads (one descriptor for the W block, one for A): the
   // compiler does not re-issue them next to their use, so they stay in flight
@@ -90,8 +96,8 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
   const __amdgpu_buffer_rsrc_t ares =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(g.A), 0, 0x7fffffff, 0x00020000);
   // byte offsets of this lane's fragments of step 0 (n-tiles 2w and 2w+1)
-  const int wv0 = ((w * 2) * S + kb / KS) * (KS * 32) + lane * 16;
-  const int wv1 = wv0 + S * (KS * 32);
+  const int wv0 = ((EPI == EPI_SWIGLU ? w : w * 2) * S + kb / KS) * (KS * 32) + lane * 16;
+  const int wv1 = wv0 + (EPI == EPI_SWIGLU ? g.N / 32 : 1) * S * (KS * 32);
   int av[Tile<MT>::PER_THREAD];
   int aoff[Tile<MT>::PER_THREAD];
 #pragma unroll
@@ -182,7 +188,17 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
 #undef GEMM_STEP
 
   // lane holds C[mt*16 + lg*4 + i][n0 + w*32 + t*16 + ln]
-  if constexpr (EPI == EPI_PARTIAL) {
+  if constexpr (EPI == EPI_SWIGLU) {
+    // t = 0: gate column (tb + w)*16 + ln, t = 1: the matching up column
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = m0 + mt * 16 + lg * 4 + i;
+        const float a = acc[mt][0][i];
+        if (m < g.M) g.out[(int64_t)m * g.ld_out + (tb + w) * 16 + ln] = f2bf(a / (1.f + expf(-a)) * acc[mt][1][i]);
+      }
+  } else if constexpr (EPI == EPI_PARTIAL) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
@@ -255,6 +271,9 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   const bool exact = (int64_t)g.kper * splits == g.K;
   if (epi == EPI_ARGMAX) {
     k_gemm<MT, 0, EPI_ARGMAX><<<grid, 256, 0, st>>>(g);
+  } else if (epi == EPI_SWIGLU) {
+    if (steps == 64) k_gemm<MT, 64, EPI_SWIGLU><<<grid, 256, 0, st>>>(g);
+    else k_gemm<MT, 0, EPI_SWIGLU><<<grid, 256, 0, st>>>(g);
   } else if (exact && steps == 4) {
     k_gemm<MT, 4, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
   } else if (exact && steps == 8) {
@@ -263,6 +282,12 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
     k_gemm<MT, 12, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
   } else if (exact && steps == 16) {
     k_gemm<MT, 16, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+  } else if (exact && steps == 32) {
+    k_gemm<MT, 32, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+  } else if (exact && steps == 48) {
+    k_gemm<MT, 48, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+  } else if (exact && steps == 64) {
+    k_gemm<MT, 64, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
   } else {
     k_gemm<MT, 0, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
   }

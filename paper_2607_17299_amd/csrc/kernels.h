@@ -36,6 +36,8 @@ struct GemmArgs {
   const int32_t* a_rows;  // nullable: A row m -> a_rows[m]
   const bf16_t* Wp;  // weights in MFMA fragment order (launch_pack_weights)
   int M, N, K, kper;
+  bf16_t* out;       // EPI_SWIGLU: silu(gate) * up, bf16 [M][ld_out]
+  int64_t ld_out;
   float* P;  // partial sums [split][M][N]
   // argmax epilogue (split == 1): per (row, 128-column block) best value and index
   float* logits;  // nullable [M][ld_logits]
@@ -44,7 +46,7 @@ struct GemmArgs {
   int32_t* amax_i;
 };
 
-enum { EPI_PARTIAL = 0, EPI_ARGMAX = 1 };
+enum { EPI_PARTIAL = 0, EPI_ARGMAX = 1, EPI_SWIGLU = 2 };
 
 struct AttnArgs {
   const bf16_t* q;  // [rows][n_q_heads * head_dim]

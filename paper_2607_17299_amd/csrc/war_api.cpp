@@ -101,7 +101,7 @@ struct war_model {
   DevBuf wts;  // owned copy of every weight (matrices packed)
   int max_rows;
   // workspace
-  DevBuf h, u, q, o, P, cos_t, sin_t, inv_freq, amax_v, amax_i;
+  DevBuf h, u, q, o, y, P, cos_t, sin_t, inv_freq, amax_v, amax_i;
   DevBuf rows_i32;  // tok, pos, active, row_req  [4][max_rows]
   DevBuf reqs_i32;  // seq, pos0, ntok, row0      [4][n_req_cap]
   DevBuf segs_i32;  // begin, count, req, rb      [4][n_seg_cap]
@@ -227,13 +227,9 @@ Split pick_split(int M, int N, int K, int64_t cap_elems) {
   const int mt = gemm_mt(M);
   const int mblocks = cdiv_i(M, mt * 16);
   const int base = (N / 128) * mblocks;
-  for (int steps : {16, 12, 8, 4}) {
-    const int kper = steps * 64;
-    if (K % kper) continue;
-    const int s = K / kper;
-    if ((int64_t)base * s >= 192 || steps == 4) {
-      if ((int64_t)s * M * N <= cap_elems) return {s, kper};
-    }
+  for (int s = 1; s <= 64; ++s) {
+    if (K % (s * 64)) continue;
+    if ((int64_t)base * s >= 192 && (int64_t)s * M * N <= cap_elems) return {s, K / s};
   }
   // fall back: one split per 1024 of K (runtime-loop kernel)
   int s = std::max(1, K / 1024);
@@ -245,7 +241,7 @@ Split pick_split(int M, int N, int K, int64_t cap_elems) {
 // One projection: P[split][M][N] = A x W^T (or the LM-head argmax epilogue).
 war_status gemm(war_model* m, const bf16_t* A, int lda, const int32_t* a_rows, const bf16_t* Wp,
                 int M, int N, int K, int* splits_out, hipStream_t st, bool argmax = false,
-                float* logits = nullptr) {
+                float* logits = nullptr, bf16_t* swiglu_out = nullptr) {
   GemmArgs g{};
   g.A = A;
   g.lda = lda;
@@ -257,12 +253,17 @@ war_status gemm(war_model* m, const bf16_t* A, int lda, const int32_t* a_rows, c
   Split sp{1, K};
   if (!argmax) sp = pick_split(M, N, K, (int64_t)(m->P.bytes / 4));
   g.kper = sp.kper;
+  // SwiGLU in the epilogue when one split covers K (else the caller reduces)
+  const bool fuse = swiglu_out && sp.s == 1;
+  g.out = swiglu_out;
+  g.ld_out = N / 2;
   g.P = m->P.as<float>();
   g.logits = logits;
   g.ld_logits = N;
   g.amax_v = m->amax_v.as<float>();
   g.amax_i = m->amax_i.as<int32_t>();
-  launch_gemm(g, argmax ? EPI_ARGMAX : EPI_PARTIAL, sp.s, st);
+  launch_gemm(g, argmax ? EPI_ARGMAX : fuse ? EPI_SWIGLU : EPI_PARTIAL, sp.s, st);
+  if (swiglu_out && !fuse) launch_swiglu(M, sp.s, g.P, N / 2, swiglu_out, st);
   if (splits_out) *splits_out = sp.s;
   return WAR_OK;
 }
@@ -277,6 +278,7 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
   bf16_t* u = m->u.as<bf16_t>();
   bf16_t* q = m->q.as<bf16_t>();
   bf16_t* o = m->o.as<bf16_t>();
+  bf16_t* y = m->y.as<bf16_t>();
   float* P = m->P.as<float>();
   Profiler& pf = m->prof;
   {
@@ -319,16 +321,12 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
       launch_residual_norm(R, s, P, md.d, L.ffn_norm, md.eps, h, u, st);
     }
     {
-      Timed t(pf, st, "gemm_gate_up");
-      gemm(m, u, md.d, nullptr, L.w_gate_up, R, 2 * md.F, md.d, &s, st);
-    }
-    {
-      Timed t(pf, st, "swiglu");
-      launch_swiglu(R, s, P, md.F, u, st);
+      Timed t(pf, st, "gemm_gate_up_swiglu");
+      gemm(m, u, md.d, nullptr, L.w_gate_up, R, 2 * md.F, md.d, &s, st, false, nullptr, y);
     }
     {
       Timed t(pf, st, "gemm_down");
-      gemm(m, u, md.F, nullptr, L.w_down, R, md.d, md.F, &s, st);
+      gemm(m, y, md.F, nullptr, L.w_down, R, md.d, md.F, &s, st);
     }
     const bf16_t* gnext = l + 1 < m->cfg.n_layers ? m->layers[l + 1].attn_norm : m->final_norm;
     {
@@ -486,6 +484,7 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
   ok(m->u.ensure((size_t)R * wide * 2));
   ok(m->q.ensure((size_t)R * md.nq * md.hd * 2));
   ok(m->o.ensure((size_t)R * md.nq * md.hd * 2));
+  ok(m->y.ensure((size_t)R * md.F * 2));
   const int64_t pneed = std::max<int64_t>((int64_t)R * std::max(md.qkv, 2 * md.F), 1);
   ok(m->P.ensure((size_t)std::max(kPartialCap, pneed) * 4));
   ok(m->cos_t.ensure((size_t)R * md.hd / 2 * 4));
@@ -513,7 +512,7 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
 
 void war_model_destroy(war_model* m) {
   if (!m) return;
-  for (DevBuf* b : {&m->wts, &m->h, &m->u, &m->q, &m->o, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
+  for (DevBuf* b : {&m->wts, &m->h, &m->u, &m->q, &m->o, &m->y, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
                     &m->amax_v, &m->amax_i, &m->rows_i32, &m->reqs_i32, &m->segs_i32, &m->n_items,
                     &m->items, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
     b->release();
