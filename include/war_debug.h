@@ -23,7 +23,9 @@ war_status war_debug_mfma16(const void* A, const void* B, float* C, void* stream
  * values).  Names: "h" fp32 residual [rows][d]; "u" bf16 last norm or SwiGLU
  * output; "q" bf16 rotated queries [rows][nq*hd]; "o" bf16 attention output
  * [rows][nq*hd]; "P" fp32 split-K partials; "pm", "pl", "po" attention
- * partials; "rows", "reqs", "items" step metadata.  The pointer stays valid
+ * partials; "rows", "reqs", "items" step metadata; "order" the attention work
+ * order and "n_items" its counts (item slots, ordinary units, shared-prefix
+ * units).  The pointer stays valid
  * until the next call on the model. */
 war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes);
 

@@ -106,6 +106,7 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
   __shared__ int sh[16];
   __shared__ int s_fail;
   __shared__ int s_ctx[kBT], s_dl[kBT];
+  __shared__ int s_pg0[kBT], s_nch[kBT], s_seq[kBT], s_shr[kBT], s_noff[kBT], s_run[kBT];
   const int t = threadIdx.x;
   const int kp1 = a.k_max + 1;
   __shared__ int s_bad;
@@ -161,9 +162,84 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
     m.seg_req[t] = t;
     m.seg_rb[t] = 0;
     for (int c = 0; c < nch; ++c) m.items[ioff + c] = make_int4(t, 0, c, 0);
+    s_pg0[t] = (!fail && ctx > 0) ? p.table[(int64_t)s * p.max_pages] : -1 - t;
+    s_nch[t] = nch;
+    s_seq[t] = s;
+    s_shr[t] = 0x7fffffff;
+  }
+  __syncthreads();
+  // Groups: consecutive requests whose first page is the same physical page
+  // (forked siblings).  The keys a group shares are the whole pages every
+  // member has in common with the first member, within every member's context
+  // (so visible to every row of the step).
+  int L = t, g = 1;
+  bool regular = true;
+  if (t < a.B) {
+    while (L > 0 && s_pg0[L - 1] == s_pg0[t]) --L;
+    while (L + g < a.B && s_pg0[L + g] == s_pg0[L]) {
+      regular = regular && s_nch[L + g] == s_nch[L];
+      ++g;
+    }
+    if (g > 1 && nch > 0) {
+      const int np = min(s_ctx[t], s_ctx[L]) / p.page_size;
+      const int32_t* rb = p.table + (int64_t)s_seq[t] * p.max_pages;
+      const int32_t* rl = p.table + (int64_t)s_seq[L] * p.max_pages;
+      int c = 0;
+      while (c < np && rb[c] == rl[c]) ++c;
+      atomicMin(&s_shr[L], c * p.page_size);
+    }
+  }
+  __syncthreads();
+  // Shared-prefix units: the whole attention chunks a group shares are attended
+  // once per run of consecutive members whose live rows (G per token) fit one
+  // row block together; the unit writes every member's partial.  The first
+  // member of a run owns it (item .w = members); the others' items for those
+  // chunks are never scheduled (.w = -1).  Ordinary items keep .w = 0.
+  const int RBs = a.rb;
+  if (t < a.B && a.cascade && L == t && g > 1 && nch > 0 && s_shr[t] >= a.chunk) {
+    int j0 = 0, rows = 0;
+    for (int jj = 0; jj < g; ++jj) {
+      const int rj = a.G * (s_dl[t + jj] + 1);
+      if (jj > j0 && rows + rj > RBs) {
+        s_run[t + j0] = jj - j0;
+        j0 = jj;
+        rows = 0;
+      }
+      rows += rj;
+      s_run[t + jj] = 0;
+    }
+    s_run[t + j0] = g - j0;
+  }
+  __syncthreads();
+  int nsc = 0;
+  if (t < a.B && a.cascade && g > 1 && nch > 0 && s_shr[L] >= a.chunk) nsc = min(s_shr[L] / a.chunk, nch);
+  const int j = t - L;
+  const int run = nsc > 0 ? s_run[t] : 0;  // members of the run this request owns (0: not an owner)
+  if (t < a.B && nsc > 0)
+    for (int c = 0; c < nsc; ++c) m.items[ioff + c].w = run > 0 ? run : -1;
+  const int n_mine = (t < a.B) ? nch - nsc + (run > 0 ? nsc : 0) : 0;
+  int n_units;
+  const int noff = block_excl_scan(n_mine, sh, &n_units);
+  if (t < a.B) s_noff[t] = noff;
+  __syncthreads();
+  // Work order.  A group without shared units whose members have equal chunk
+  // counts gets its items interleaved chunk-major (the members read a shared
+  // chunk at the same time, so later readers find it in cache); otherwise
+  // request order, a run's shared units first.
+  if (t < a.B && nch > 0) {
+    if (nsc == 0 && g > 1 && regular) {
+      for (int c = 0; c < nch; ++c) m.order[s_noff[L] + c * g + j] = ioff + c;
+    } else {
+      int o = noff;
+      if (run > 0)
+        for (int c = 0; c < nsc; ++c) m.order[o++] = ioff + c;
+      for (int c = nsc; c < nch; ++c) m.order[o++] = ioff + c;
+    }
   }
   if (t == 0) {
     m.n_items[0] = n_items;
+    m.n_items[1] = n_units;
+    m.n_items[2] = 0;
     if (fail && !s_bad) p.scalars[1] |= ERR_NO_PAGES;
     if (!fail) p.scalars[0] = fc - total;
   }

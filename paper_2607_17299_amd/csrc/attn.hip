@@ -55,22 +55,52 @@ k_attn(AttnArgs a) {
   __shared__ float s_o[RB * OST];
   __shared__ __attribute__((aligned(16))) bf16_t s_q[QLDS ? RB * QST : 8];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
-  const int total = a.meta.n_items[0] * a.n_kv_heads;
+  const int total = (a.meta.order ? a.meta.n_items[1] : a.meta.n_items[0]) * a.n_kv_heads;
   const int P = a.kv.page_size;
   // key row of this lane in S^T tile t (within a 32-key block); tile 1 adds 4
   const int kk0 = (ln >> 2) * 8 + (ln & 3);
 
   for (int it = blockIdx.x; it < total; it += gridDim.x) {
-    const int item = it / a.n_kv_heads, kvh = it % a.n_kv_heads;
+    // units in work order; with 8 kv-heads (a multiple of 8 in general) every
+    // unit of one kv-head runs on the same XCD, so items that are neighbours in
+    // the order (the same prefix chunk of sibling requests) share its L2
+    const int slot = it / a.n_kv_heads, kvh = it % a.n_kv_heads;
+    const int item = a.meta.order ? a.meta.order[slot] : slot;
     const int4 itm = a.meta.items[item];
     const int b = itm.x, t0 = itm.y * a.TB, chunk = itm.z;
+    // a shared-prefix unit (.w = n > 0) covers the live rows of requests
+    // b .. b+n-1, one after the other, and sees every key of its chunk (the
+    // shared keys precede every member's rows): no causal mask
+    const bool shared = itm.w > 0;
+    const int nmem = shared ? itm.w : 1;
     const int seq = a.meta.req_seq[b], pos0 = a.meta.req_pos0[b];
     const int row0 = a.meta.req_row0[b];
     const int nt = min(a.TB, a.meta.req_ntok[b] - t0);
-    const int nrows = nt * a.G;
-    const int last_pos = pos0 + t0 + nt - 1;
+    int nrows = nt * a.G;
+    if (shared)
+      for (int jm = 1; jm < nmem; ++jm) nrows += min(a.TB, a.meta.req_ntok[b + jm]) * a.G;
+    const int last_pos = shared ? (chunk + 1) * a.chunk - 1 : pos0 + t0 + nt - 1;
+    const int qpos0 = shared ? last_pos + 1 : pos0 + t0;  // smallest row position
     const int S = last_pos + 1;
     const int kbeg = chunk * a.chunk, kend = min(S, kbeg + a.chunk);
+    // row r -> (query row, query head) and its partial row; false if r is not live
+    auto row_src = [&](int r, int& qrow, int& h, int64_t& prow) -> bool {
+      if (r >= nrows) return false;
+      int jm = 0, lr = r;
+      if (shared) {
+        int nr = min(a.TB, a.meta.req_ntok[b]) * a.G;
+        while (lr >= nr) {
+          lr -= nr;
+          ++jm;
+          nr = min(a.TB, a.meta.req_ntok[b + jm]) * a.G;
+        }
+      }
+      qrow = a.meta.req_row0[b + jm] + t0 + lr / a.G;
+      h = kvh * a.G + lr % a.G;
+      const int pitem = shared ? a.meta.seg_begin[b + jm] + chunk : item;
+      prow = ((int64_t)pitem * a.n_kv_heads + kvh) * a.prb + lr;
+      return true;
+    };
 
     // queries (B operand of S^T): lane (n = ln, g = lg) of row tile rt
     int rpos[NR];
@@ -78,16 +108,16 @@ k_attn(AttnArgs a) {
 #pragma unroll
     for (int rt = 0; rt < NR; ++rt) {
       const int r = rt * 16 + ln;
-      rpos[rt] = r < nrows ? pos0 + t0 + r / a.G : last_pos;
+      rpos[rt] = (!shared && r < nrows) ? pos0 + t0 + r / a.G : last_pos;
     }
     if constexpr (QLDS) {
       for (int e = tid; e < RB * (HD / 8); e += 256) {
         const int r = e / (HD / 8), c = (e % (HD / 8)) * 8;
         uint4 v = make_uint4(0, 0, 0, 0);
-        if (r < nrows) {
-          const int ti = t0 + r / a.G, h = kvh * a.G + r % a.G;
-          v = *reinterpret_cast<const uint4*>(a.q + (int64_t)(row0 + ti) * a.q_stride + h * HD + c);
-        }
+        int qrow, h;
+        int64_t prow;
+        if (row_src(r, qrow, h, prow))
+          v = *reinterpret_cast<const uint4*>(a.q + (int64_t)qrow * a.q_stride + h * HD + c);
         *reinterpret_cast<uint4*>(&s_q[r * QST + c]) = v;
       }
       __syncthreads();
@@ -95,9 +125,10 @@ k_attn(AttnArgs a) {
 #pragma unroll
       for (int rt = 0; rt < (QLDS ? 1 : NR); ++rt) {
         const int r = rt * 16 + ln;
-        if (r < nrows) {
-          const int ti = t0 + r / a.G, h = kvh * a.G + r % a.G;
-          const bf16_t* qp = a.q + (int64_t)(row0 + ti) * a.q_stride + h * HD + lg * DPL;
+        int qrow, h;
+        int64_t prow;
+        if (row_src(r, qrow, h, prow)) {
+          const bf16_t* qp = a.q + (int64_t)qrow * a.q_stride + h * HD + lg * DPL;
 #pragma unroll
           for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + j * 8));
         } else {
@@ -153,7 +184,7 @@ k_attn(AttnArgs a) {
 
     auto compute_block = [&](const KVFrag<HD>& f, int kb) {
       // keys of this block above the smallest row position need the causal mask
-      const bool tail = kb + 31 > pos0 + t0;
+      const bool tail = kb + 31 > qpos0;
       if constexpr (QLDS) asm volatile("" ::: "memory");  // re-read Q from LDS each block
       // phase 1: scores of every row tile (the K fragments die after this)
       float sc[NR][8];
@@ -297,20 +328,27 @@ k_attn(AttnArgs a) {
       __syncthreads();
     }
     // partial of the live rows only: [item][kvh][row][dim] with row stride HD
-    const int64_t pbase = ((int64_t)item * a.n_kv_heads + kvh) * RB;
+    // (a shared-prefix unit writes each member's rows into that member's item)
     for (int e = tid; e < nrows * (HD / 4); e += 256) {
       const int r = e / (HD / 4), d4 = (e % (HD / 4)) * 4;
+      int qrow, h;
+      int64_t prow;
+      if (!row_src(r, qrow, h, prow)) continue;
       const float* src = &s_o[r * OST + d4];
-      *reinterpret_cast<float4*>(&a.po[(pbase + r) * HD + d4]) = make_float4(src[0], src[1], src[2], src[3]);
+      *reinterpret_cast<float4*>(&a.po[prow * HD + d4]) = make_float4(src[0], src[1], src[2], src[3]);
     }
     if (tid < nrows) {
       const int r = tid;
-      const float mm = fmaxf(fmaxf(s_m[0][r], s_m[1][r]), fmaxf(s_m[2][r], s_m[3][r]));
-      const float mu = mm == -INFINITY ? 0.f : mm;
-      float l = 0.f;
-      for (int ww = 0; ww < 4; ++ww) l += s_l[ww][r] * exp2f(s_m[ww][r] - mu);
-      a.pm[pbase + r] = mm;
-      a.pl[pbase + r] = l;
+      int qrow, h;
+      int64_t prow;
+      if (row_src(r, qrow, h, prow)) {
+        const float mm = fmaxf(fmaxf(s_m[0][r], s_m[1][r]), fmaxf(s_m[2][r], s_m[3][r]));
+        const float mu = mm == -INFINITY ? 0.f : mm;
+        float l = 0.f;
+        for (int ww = 0; ww < 4; ++ww) l += s_l[ww][r] * exp2f(s_m[ww][r] - mu);
+        a.pm[prow] = mm;
+        a.pl[prow] = l;
+      }
     }
     __syncthreads();
   }

@@ -89,7 +89,10 @@ struct StepMeta {
   int32_t* req_ntok;
   int32_t* req_row0;
   int4* items;
-  int32_t* n_items;     // [1]
+  // nullable: the attention work order, n_items[1] item slots.  An item with
+  // .w > 0 is a shared-prefix unit covering the rows of requests x .. x+w-1.
+  int32_t* order;
+  int32_t* n_items;     // [0] item slots, [1] units in the work order
   int32_t* seg_begin;   // [n_segs]
   int32_t* seg_count;   // [n_segs]
   int32_t* seg_req;     // [n_segs]

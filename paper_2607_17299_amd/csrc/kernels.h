@@ -21,6 +21,9 @@ struct KvGeom {
 
 struct VerifySetupArgs {
   int B, k_max, vocab, chunk;
+  int G;        // query heads per kv-head
+  int rb;       // attention row block of the step (rows per unit)
+  int cascade;  // 1: plan shared-prefix attention units for forked siblings
   const int32_t* seq_ids;
   const int32_t* ctx_lens;
   const int32_t* last_tokens;
@@ -57,6 +60,7 @@ struct AttnArgs {
   int max_pages;
   StepMeta meta;
   int G, TB, chunk, n_kv_heads;
+  int prb;           // rows per (item, kv-head) in the partials (the step's row block)
   float scale_log2;  // log2(e) / sqrt(head_dim)
   float* pm;         // [item][kvh][RB]
   float* pl;         // [item][kvh][RB]

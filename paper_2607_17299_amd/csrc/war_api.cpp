@@ -105,7 +105,7 @@ struct war_model {
   DevBuf rows_i32;  // tok, pos, active, row_req  [4][max_rows]
   DevBuf reqs_i32;  // seq, pos0, ntok, row0      [4][n_req_cap]
   DevBuf segs_i32;  // begin, count, req, rb      [4][n_seg_cap]
-  DevBuf n_items, items, pm, pl, po, a_rows;
+  DevBuf n_items, items, order, pm, pl, po, a_rows;
   int n_req_cap, n_seg_cap;
   std::vector<int32_t> h_stage;  // host staging for prefill metadata
   DevBuf stage_dev;              // device copy of per-prefill host arrays
@@ -126,6 +126,7 @@ struct war_model {
     m.req_ntok = q4 + 2 * n_req_cap;
     m.req_row0 = q4 + 3 * n_req_cap;
     m.items = items.as<int4>();
+    m.order = order.as<int32_t>();
     m.n_items = n_items.as<int32_t>();
     int32_t* s4 = segs_i32.as<int32_t>();
     m.seg_begin = s4;
@@ -147,6 +148,7 @@ struct war_kv_pool {
   int64_t free_lb;  // host lower bound of the device free count
   bool pending = false;
   int pending_B = 0;
+  bool forked = false;  // some sequences may share pages (war_kv_fork was called)
 };
 
 namespace {
@@ -308,6 +310,7 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
       Timed t(pf, st, "attention");
       launch_attn(a, RB, md.hd, attn_grid, st);
     }
+
     {
       Timed t(pf, st, "attn_combine");
       launch_attn_combine(a, RB, md.hd, n_segs, st);
@@ -360,6 +363,7 @@ AttnArgs attn_args(war_model* m, war_kv_pool* p, int TB, int chunk) {
 
 war_status ensure_items(war_model* m, int64_t n_items, int RB) {
   HIPCHK(m->items.ensure(std::max<int64_t>(n_items, 1) * sizeof(int4)));
+  HIPCHK(m->order.ensure(std::max<int64_t>(n_items, 1) * sizeof(int32_t)));
   const int64_t pr = std::max<int64_t>(n_items, 1) * m->md.nkv * RB;
   HIPCHK(m->pm.ensure(pr * sizeof(float)));
   HIPCHK(m->pl.ensure(pr * sizeof(float)));
@@ -514,7 +518,7 @@ void war_model_destroy(war_model* m) {
   if (!m) return;
   for (DevBuf* b : {&m->wts, &m->h, &m->u, &m->q, &m->o, &m->y, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
                     &m->amax_v, &m->amax_i, &m->rows_i32, &m->reqs_i32, &m->segs_i32, &m->n_items,
-                    &m->items, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
+                    &m->items, &m->order, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
     b->release();
   if (m->pinned) (void)hipHostFree(m->pinned);
   for (hipEvent_t e : m->prof.pool) (void)hipEventDestroy(e);
@@ -647,6 +651,7 @@ war_status war_kv_fork(war_kv_pool* p, int32_t src_seq, int32_t dst_seq, int32_t
   CHECK(hs >= npg, "fork source holds fewer pages");
   launch_fork(p->dev, src_seq, dst_seq, npg, st);
   HIPCHK(hipGetLastError());
+  if (npg > 0) p->forked = true;
   return WAR_OK;
 }
 
@@ -744,12 +749,16 @@ war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_
   va.last_tokens = last_tokens;
   va.draft_tokens = draft_tokens;
   va.draft_lens = draft_lens;
+  va.G = G;
+  va.rb = RB;
+  va.cascade = p->forked && B > 1 ? 1 : 0;  // shared-prefix units for forked siblings
   {
     Timed t(m->prof, st, "verify_setup");
     launch_verify_setup(p->dev, va, m->meta(), st);
   }
 
   AttnArgs a = attn_args(m, p, kp1, chunk);
+  a.prb = RB;
   // persistent grid = resident capacity: 2 workgroups per CU
   const int grid = (int)std::min<int64_t>(max_items * m->md.nkv, 512);
   s = run_layers(m, p, R, a, RB, grid, B, st);
@@ -904,6 +913,8 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
     HIPCHK(hipStreamSynchronize(st));  // host vectors go out of scope below
 
     AttnArgs a = attn_args(m, p, TB, chunk);
+    a.meta.order = nullptr;  // prefill items run in list order
+    a.prb = RB;
     const int grid = (int)std::min<int64_t>((int64_t)ni * m->md.nkv, 512);
     s = run_layers(m, p, R, a, RB, std::max(grid, 1), nseg, st);
     if (s != WAR_OK) return s;
@@ -978,7 +989,7 @@ war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64
   const DevBuf* b = n == "h" ? &m->h : n == "u" ? &m->u : n == "q" ? &m->q : n == "o" ? &m->o
                   : n == "P" ? &m->P : n == "pm" ? &m->pm : n == "pl" ? &m->pl : n == "po" ? &m->po
                   : n == "rows" ? &m->rows_i32 : n == "reqs" ? &m->reqs_i32 : n == "items" ? &m->items
-                  : nullptr;
+                  : n == "order" ? &m->order : n == "n_items" ? &m->n_items : nullptr;
   CHECK(b, "unknown workspace buffer");
   *ptr = b->p;
   *bytes = (int64_t)b->bytes;

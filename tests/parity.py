@@ -60,3 +60,16 @@ def compare_request(o_logits: np.ndarray, g_logits: np.ndarray, drafts, o_accept
     else:
         report.append(f"{tag}: accept/next ({g_accept},{g_next}) vs oracle ({o_accept},{o_next}) at a near-tie")
     return {"err": err, "min_gap": float(gap.min())}
+
+
+def shared_units(rows, rb):
+    """Runs of consecutive siblings whose live rows fit one row block together
+    (the packing the step setup does); returns the run lengths."""
+    runs, cur, n = [], 0, 0
+    for r in rows:
+        if n and cur + r > rb:
+            runs.append(n)
+            cur, n = 0, 0
+        cur += r
+        n += 1
+    return runs + [n]

@@ -20,7 +20,7 @@ import torch
 from oracle.decoder import RequestKV, Weights, forward_block
 from oracle.verify import greedy_decode, prefill_request, verify_request
 from paper_2607_17299_amd import harness, synth
-from parity import compare_request, fp32_drift_tol
+from parity import compare_request, fp32_drift_tol, shared_units
 
 pytestmark = pytest.mark.gpu
 KV_SEED = 9
@@ -152,23 +152,26 @@ def test_reduced_depth_prefill_append(large2):
         np.testing.assert_allclose(g[1][:, ctxs[b]:], V[:, ctxs[b]:], atol=3e-2, rtol=2e-2)
 
 
-def test_reduced_depth_multi_turn(large2):
+@pytest.mark.parametrize("prefix", [256, 2048])
+def test_reduced_depth_multi_turn(large2, prefix):
     """The multi-turn append path on the full widths at 2 layers: 2 groups x 2
-    trajectories whose cached contexts share a forked 256-token prefix plus
-    200 private tokens (456 cached: not a page multiple), a 300-token
+    trajectories whose cached contexts share a forked prefix (256 tokens: less
+    than an attention chunk; 2048: two whole chunks, attended once per sibling
+    pair) plus 200 private tokens (not a page multiple), a 300-token
     observation appended to each (prefill chunks span the 512-row workspace),
     then one k = 4 verify step.  Trajectory 0 drafts the oracle's own greedy
     continuation (all accepted), trajectory 1 the same with its second draft
     replaced (one accepted), the others draft from the suffix drafter."""
     war, cfg, model, W = large2["war"], large2["cfg"], large2["model"], large2["W"]
-    mt = harness.multi_turn_inputs(seed=11, groups=2, per_group=2, prefix=256, private=200,
+    mt = harness.multi_turn_inputs(seed=11, groups=2, per_group=2, prefix=prefix, private=200,
                                    n_new=300, vocab=cfg.vocab)
     pool = harness.multi_turn_pool(cfg, mt, 4)
     harness.load_multi_turn(pool, cfg, mt, KV_SEED)
     bt = pool.block_tables.cpu().numpy()
-    np.testing.assert_array_equal(bt[0, :16], bt[1, :16])        # the prefix pages are shared
-    np.testing.assert_array_equal(bt[2, :16], bt[3, :16])
-    assert len(set(bt[0, 16:29]) & set(bt[1, 16:29])) == 0        # the private ones are not
+    npg = prefix // 16
+    np.testing.assert_array_equal(bt[0, :npg], bt[1, :npg])      # the prefix pages are shared
+    np.testing.assert_array_equal(bt[2, :npg], bt[3, :npg])
+    assert len(set(bt[0, npg:npg + 13]) & set(bt[1, npg:npg + 13])) == 0   # the private ones are not
     nxt, ctx_d, last = harness.multi_turn_append(model, pool, mt, last_logits=True)
     torch.cuda.synchronize()
     assert ctx_d.cpu().tolist() == [mt.cached + mt.n_new] * mt.n
@@ -202,6 +205,14 @@ def test_reduced_depth_multi_turn(large2):
     st = harness.Step(mt.seq_ids, base.ctx_lens, onext, drafts, 4)
     ds = harness.DeviceStep(st, with_logits=True, vocab=cfg.vocab)
     ds.verify(model, pool, logits=True)
+    torch.cuda.synchronize()
+    n_items = war.debug_workspace(model, "n_items", torch.int32, (2,)).cpu().tolist()
+    # 2048 shared tokens = 2 chunks of 1024: attended once per run of siblings
+    # whose live rows fit one 32-row block together
+    runs = [shared_units([4 * (len(d) + 1) for d in st.drafts[g:g + 2]], 32) for g in (0, 2)]
+    saved = sum(2 * (2 - len(r)) for r in runs) if prefix == 2048 else 0
+    assert n_items == [n_items[0], n_items[0] - saved], (n_items, runs)
+    print(f"shared-prefix runs {runs}: {saved} units saved")
     ds.commit(pool, discard=False)
     torch.cuda.synchronize()
     glog = ds.logits.cpu().numpy().reshape(st.B, 5, cfg.vocab)

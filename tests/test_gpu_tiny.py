@@ -14,7 +14,7 @@ from oracle.pages import PagePool
 from oracle.verify import commit_request, greedy_decode, prefill_request, verify_request
 from paper_2607_17299_amd import synth
 from paper_2607_17299_amd.drafter import SuffixDrafter
-from parity import compare_request
+from parity import compare_request, shared_units
 
 pytestmark = pytest.mark.gpu
 CFG = synth.TINY
@@ -309,6 +309,81 @@ def test_mode_switching_is_stateless(tiny):
         np.testing.assert_allclose(g[0], K, atol=2e-2, rtol=2e-2)
         np.testing.assert_allclose(g[1], V, atol=2e-2, rtol=2e-2)
     print(f"\nmode switching: reported {report}")
+
+
+def test_shared_prefix_cascade(tiny):
+    """Forked siblings: requests 0-2 share a 1056-token prefix (war_kv_fork of
+    whole pages) and each appends 100 private tokens; request 3 is unrelated.
+    Two verify steps with ragged drafts (2, 1, 4, 4 tokens: the oracle's own
+    continuation, request 2 with a wrong second draft): requests 0 and 1 have
+    6 + 4 live rows and attend their shared chunk in one unit, request 2 (10
+    rows) in its own.  Logits, accepts and the committed KV are compared with
+    the oracle, which runs every request on its own."""
+    war, model, W = tiny["war"], tiny["model"], tiny["W"]
+    prefix = synth.uniform_tokens(901, 1056, CFG.vocab)
+    priv = [synth.uniform_tokens(910 + b, 100, CFG.vocab) for b in range(3)] + \
+           [synth.uniform_tokens(920, 500, CFG.vocab)]
+    B, k = 4, 4
+    dls = [2, 1, 4, 4]
+    pool = war.Pool(CFG, 512, B, 128)
+    t = lambda a: torch.as_tensor(np.asarray(a), dtype=torch.int32).to(DEV)
+    c0 = t([0])
+    war.prefill_append(model, pool, t([0]), c0, [len(prefix)], t(prefix), t([0]), None)
+    for b in (1, 2):
+        pool.fork(0, b, len(prefix))
+    ctx = t([len(prefix)] * 3 + [0])
+    nxt = t([0] * B)
+    war.prefill_append(model, pool, t(range(B)), ctx, [len(x) for x in priv], t(np.concatenate(priv)), nxt, None)
+    torch.cuda.synchronize()
+    bt = pool.block_tables.cpu().numpy()
+    assert (bt[1, :66] == bt[0, :66]).all() and (bt[2, :66] == bt[0, :66]).all()
+    # oracle: each request on its own
+    base = RequestKV(CFG)
+    prefill_request(CFG, W, base, prefix)
+    kvs, pending = [], []
+    for b in range(B):
+        kv = RequestKV(CFG, list(base.layers)) if b < 3 else RequestKV(CFG)
+        r = prefill_request(CFG, W, kv, priv[b])
+        kvs.append(kv)
+        pending.append(r["next"])
+    seq = t(range(B))
+    report = []
+    G = CFG.n_q_heads // CFG.n_kv_heads
+    assert shared_units([G * (d + 1) for d in dls[:3]], 16) == [2, 1]
+    for step in range(2):
+        drafts = [greedy_decode(CFG, W, copy.deepcopy(kvs[b]), pending[b], dls[b]) for b in range(B)]
+        drafts[2][1] = (drafts[2][1] + 1) % CFG.vocab
+        dt = np.zeros((B, k), np.int32)
+        for b, d in enumerate(drafts):
+            dt[b, :len(d)] = d
+        acc, nx = t([0] * B), t([0] * B)
+        logits = torch.zeros((B * (k + 1), CFG.vocab), device=DEV)
+        war.verify_step(model, pool, seq, ctx, t(pending), t(dt), t(dls), k, acc, nx, logits)
+        torch.cuda.synchronize()
+        # the plan: 2 chunks of 1024 keys for each sibling, 1 for request 3 (7
+        # slots); chunk 0 of requests 0 and 1 is one unit: 6 units
+        n_items = war.debug_workspace(model, "n_items", torch.int32, (2,)).cpu().tolist()
+        assert n_items == [7, 6], n_items
+        g_acc, g_nxt = acc.cpu().numpy(), nx.cpu().numpy()
+        glog = logits.cpu().numpy().reshape(B, k + 1, CFG.vocab)
+        o_acc = []
+        for b in range(B):
+            r = verify_request(CFG, W, kvs[b], pending[b], drafts[b])
+            compare_request(r["logits"], glog[b], drafts[b], r["accept"], r["next"], int(g_acc[b]),
+                            int(g_nxt[b]), report, f"step {step} req {b}")
+            commit_request(kvs[b], r)
+            pending[b] = r["next"]
+            o_acc.append(r["accept"])
+        assert o_acc == [2, 1, 1, 4], o_acc
+        war.kv_commit(pool, seq, ctx, t(o_acc))
+        torch.cuda.synchronize()
+        assert ctx.cpu().tolist() == [kv.length for kv in kvs]
+    for b in range(B):
+        g = pool.gather_kv(b, kvs[b].length, CFG.n_layers - 1).double().cpu().numpy()
+        K, V = kvs[b].get(CFG.n_layers - 1)
+        np.testing.assert_allclose(g[0], K, atol=2e-2, rtol=2e-2)
+        np.testing.assert_allclose(g[1], V, atol=2e-2, rtol=2e-2)
+    print(f"\nshared-prefix cascade: reported {report}")
 
 
 @pytest.mark.parametrize("mode", ["suffix", "greedy", "mixed"])
