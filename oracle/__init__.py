@@ -15,6 +15,8 @@ Modules
             reserve / commit / rollback / fork / free.
   verify    one verify step / one prefill-append for a batch, composed from the
             above in the order the method takes them.
+  sampling  sampled verification (temperature, top-k, lossless speculative
+            sampling with a deterministic drafter; uniforms are inputs).
 
 What the paper fixes (arXiv 2607.17299):
   * speculative decoding is lossless: the target model verifies drafts and the
