@@ -296,6 +296,27 @@ def main():
                                       "accepted_tokens_per_s": round(float((acc2 + 1).sum() / (ms2 / 1e3)), 1),
                                       "accept_lens": acc2.tolist()}
 
+    if not args.no_variants:
+        # sampled verification in the paper's setting (temperature 1, top-k 200),
+        # same requests and drafts; uniforms drawn once on the device
+        g = torch.Generator(device="cuda")
+        g.manual_seed(7)
+        uni = torch.rand((st.B * (st.k_max + 1), 2), generator=g, device="cuda", dtype=torch.float32)
+        for _ in range(2):
+            ds.verify_sampled(model, pool, uni)
+            ds.commit(pool, discard=True)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            ds.verify_sampled(model, pool, uni)
+            ds.commit(pool, discard=True)
+        torch.cuda.synchronize()
+        ms3 = (time.perf_counter() - t0) * 1e3 / args.steps
+        acc3 = ds.accept.cpu().numpy()
+        variants["sampled_T1_top200"] = {"ms_per_step": round(ms3, 4),
+                                         "accepted_tokens_per_s": round(float((acc3 + 1).sum() / (ms3 / 1e3)), 1),
+                                         "accept_lens": acc3.tolist()}
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the oracle on the host")

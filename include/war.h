@@ -171,6 +171,30 @@ war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_
                            int32_t* accept_lens, int32_t* next_tokens, float* logits,
                            void* stream);
 
+/* The verify step with sampled verification instead of greedy acceptance (the
+ * paper's rollouts sample: Evaluation, temperature 1.0, top-k 200; speculation
+ * stays lossless: Introduction; Background, "Why Workload Matters").  Same
+ * arguments and pool protocol as war_verify_step, plus:
+ *   uniforms     device fp32 [B * (k_max + 1)][2], each in [0, 1): for row
+ *                b*(k_max+1)+i, [0] is the acceptance test of draft i+1 and [1]
+ *                the draw made at that row.  The caller owns the randomness.
+ *   temperature  > 0
+ *   top_k        in [1, vocab]
+ * Row i's target distribution keeps the top_k largest logits (value
+ * descending, ties to the lowest token id) and takes softmax(logit / T) over
+ * them.  Draft i+1 is accepted iff uniform[0] < p_i(draft); at the first
+ * rejection next_token is drawn from p_i without the rejected draft, and after
+ * the last accepted draft from p_n; a draw with uniform v is the smallest token
+ * id whose cumulative weight (in id order) exceeds v times the total.  The
+ * logits are written to `logits` when it is not NULL, else to a workspace the
+ * model allocates on first use ([B * (k_max + 1)][vocab] fp32).  Decisions are
+ * taken in fp32. */
+war_status war_verify_step_sampled(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                                   const int32_t* ctx_lens, const int32_t* last_tokens,
+                                   const int32_t* draft_tokens, const int32_t* draft_lens, int32_t k_max,
+                                   const float* uniforms, float temperature, int32_t top_k,
+                                   int32_t* accept_lens, int32_t* next_tokens, float* logits, void* stream);
+
 /* Commit the pending verify step.
  *   accept_lens device int32 [B]; -1 discards the step.  Values are clamped
  *               to [-1, reserved capacity].

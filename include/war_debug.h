@@ -29,6 +29,15 @@ war_status war_debug_mfma16(const void* A, const void* B, float* C, void* stream
  * until the next call on the model. */
 war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes);
 
+/* The sampled-verification decision kernels alone (those war_verify_step_sampled
+ * runs after the LM head), on caller-provided rows: logits device fp32
+ * [B*(k_max+1)][V]; ntok device int32 [B] (drafts + 1; 0 = no rows); drafts
+ * device int32 [B][k_max]; uniforms, temperature, top_k and the outputs as in
+ * war_verify_step_sampled.  Synchronises the stream. */
+war_status war_debug_sample(const float* logits, int32_t V, int32_t B, int32_t k_max, const int32_t* ntok,
+                            const int32_t* drafts, const float* uniforms, float temperature, int32_t top_k,
+                            int32_t* accept_lens, int32_t* next_tokens, void* stream);
+
 /* Per-kernel timing.  war_profile(m, 1) clears the record and starts timing
  * every kernel launch of later verify/prefill calls on this model.  Each
  * launch is bracketed by a pair of HIP events on the launch stream.

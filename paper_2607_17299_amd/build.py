@@ -16,7 +16,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT = os.path.join(HERE, "libwar.so")
-SOURCES = ["alloc.hip", "gemm.hip", "attn.hip", "rows.hip", "debug.hip", "war_api.cpp"]
+SOURCES = ["alloc.hip", "gemm.hip", "attn.hip", "rows.hip", "sample.hip", "debug.hip", "war_api.cpp"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 FLAGS = ["--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",
          # packed-fp32 instructions are kept out of every kernel

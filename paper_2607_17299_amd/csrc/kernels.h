@@ -88,6 +88,20 @@ void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st);
 // W [N][K] row-major -> dst in MFMA fragment order; N % 16 == 0, K % 64 == 0
 void launch_pack_weights(const bf16_t* W, int N, int K, bf16_t* dst, hipStream_t st);
 
+// sampled verification (sample.hip)
+struct SampleArgs {
+  const float* logits;     // [B * kp1][V] fp32
+  int V;
+  const int32_t* ntok;     // per request: drafts + 1 (0: no rows)
+  const int32_t* drafts;   // [B][k_max]
+  int k_max, kp1, B;
+  const float* uniforms;   // [B * kp1][2]: acceptance test, draw
+  float temperature;
+  int top_k;
+  int32_t* row_out;        // [B * kp1][3]: accepted?, token if rejected here, token if last
+};
+void launch_sample(const SampleArgs& s, int32_t* accept_lens, int32_t* next_tokens, hipStream_t st);
+
 // attention (attn.hip)
 int attn_rows_per_block(int G, int k_rows);  // RB (16, 32 or 48)
 void launch_attn(const AttnArgs& a, int RB, int head_dim, int grid, hipStream_t st);

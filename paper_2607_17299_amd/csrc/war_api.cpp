@@ -106,6 +106,7 @@ struct war_model {
   DevBuf reqs_i32;  // seq, pos0, ntok, row0      [4][n_req_cap]
   DevBuf segs_i32;  // begin, count, req, rb      [4][n_seg_cap]
   DevBuf n_items, items, order, pm, pl, po, a_rows;
+  DevBuf logits_ws, row_out;  // sampled verification: full logits, per-row outcomes
   int n_req_cap, n_seg_cap;
   std::vector<int32_t> h_stage;  // host staging for prefill metadata
   DevBuf stage_dev;              // device copy of per-prefill host arrays
@@ -518,7 +519,7 @@ void war_model_destroy(war_model* m) {
   if (!m) return;
   for (DevBuf* b : {&m->wts, &m->h, &m->u, &m->q, &m->o, &m->y, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
                     &m->amax_v, &m->amax_i, &m->rows_i32, &m->reqs_i32, &m->segs_i32, &m->n_items,
-                    &m->items, &m->order, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
+                    &m->items, &m->order, &m->logits_ws, &m->row_out, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
     b->release();
   if (m->pinned) (void)hipHostFree(m->pinned);
   for (hipEvent_t e : m->prof.pool) (void)hipEventDestroy(e);
@@ -689,10 +690,21 @@ war_status war_kv_load(war_kv_pool* p, int32_t seq_id, int32_t layer, int32_t po
   return WAR_OK;
 }
 
-war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
-                           const int32_t* ctx_lens, const int32_t* last_tokens, const int32_t* draft_tokens,
-                           const int32_t* draft_lens, int32_t k_max, int32_t* accept_lens,
-                           int32_t* next_tokens, float* logits, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Sampling parameters of war_verify_step_sampled (nullptr uniforms: greedy).
+struct SampleParams {
+  const float* uniforms = nullptr;
+  float temperature = 1.f;
+  int top_k = 1;
+};
+
+war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                       const int32_t* ctx_lens, const int32_t* last_tokens, const int32_t* draft_tokens,
+                       const int32_t* draft_lens, int32_t k_max, int32_t* accept_lens,
+                       int32_t* next_tokens, float* logits, void* stream, const SampleParams& sp) {
   CHECK(m && p, "null model or pool");
   CHECK(same_shape(m->cfg, p->cfg), "model and pool shapes differ");
   CHECK(!p->pending, "previous verify step not committed");
@@ -764,12 +776,38 @@ war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_
   s = run_layers(m, p, R, a, RB, grid, B, st);
   if (s != WAR_OK) return s;
   int sdummy;
-  {
-    Timed t(m->prof, st, "gemm_lm_head_argmax");
-    gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, R, m->md.V, m->md.d, &sdummy,
-         st, true, logits);
-  }
-  {
+  if (sp.uniforms) {
+    // the full logits are needed: the caller's buffer, else the workspace
+    float* lg = logits;
+    if (!lg) {
+      HIPCHK(m->logits_ws.ensure((size_t)R * m->md.V * 4));
+      lg = m->logits_ws.as<float>();
+    }
+    HIPCHK(m->row_out.ensure((size_t)R * 3 * 4));
+    {
+      Timed t(m->prof, st, "gemm_lm_head");
+      gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, R, m->md.V, m->md.d, &sdummy, st, true, lg);
+    }
+    SampleArgs sa{};
+    sa.logits = lg;
+    sa.V = m->md.V;
+    sa.ntok = m->meta().req_ntok;
+    sa.drafts = draft_tokens;
+    sa.k_max = k_max;
+    sa.kp1 = kp1;
+    sa.B = B;
+    sa.uniforms = sp.uniforms;
+    sa.temperature = sp.temperature;
+    sa.top_k = sp.top_k;
+    sa.row_out = m->row_out.as<int32_t>();
+    Timed t(m->prof, st, "sample_accept");
+    launch_sample(sa, accept_lens, next_tokens, st);
+  } else {
+    {
+      Timed t(m->prof, st, "gemm_lm_head_argmax");
+      gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, R, m->md.V, m->md.d, &sdummy,
+           st, true, logits);
+    }
     Timed t(m->prof, st, "argmax_accept");
     launch_argmax_accept(B, m->meta().req_ntok, kp1, m->md.V / 128, m->amax_v.as<float>(),
                          m->amax_i.as<int32_t>(), draft_tokens, k_max, accept_lens, next_tokens, st);
@@ -779,6 +817,35 @@ war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_
   p->pending = true;
   p->pending_B = B;
   return WAR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                           const int32_t* ctx_lens, const int32_t* last_tokens, const int32_t* draft_tokens,
+                           const int32_t* draft_lens, int32_t k_max, int32_t* accept_lens,
+                           int32_t* next_tokens, float* logits, void* stream) {
+  return verify_impl(m, p, B, seq_ids, ctx_lens, last_tokens, draft_tokens, draft_lens, k_max, accept_lens,
+                     next_tokens, logits, stream, SampleParams{});
+}
+
+war_status war_verify_step_sampled(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                                   const int32_t* ctx_lens, const int32_t* last_tokens,
+                                   const int32_t* draft_tokens, const int32_t* draft_lens, int32_t k_max,
+                                   const float* uniforms, float temperature, int32_t top_k,
+                                   int32_t* accept_lens, int32_t* next_tokens, float* logits, void* stream) {
+  CHECK(m, "null model");
+  CHECK(uniforms, "null uniforms");
+  CHECK(std::isfinite(temperature) && temperature > 0.f, "temperature must be positive and finite");
+  CHECK(top_k >= 1 && top_k <= m->md.V, "top_k out of range [1, vocab]");
+  SampleParams sp;
+  sp.uniforms = uniforms;
+  sp.temperature = temperature;
+  sp.top_k = top_k;
+  return verify_impl(m, p, B, seq_ids, ctx_lens, last_tokens, draft_tokens, draft_lens, k_max, accept_lens,
+                     next_tokens, logits, stream, sp);
 }
 
 war_status war_kv_commit(war_kv_pool* p, int32_t B, const int32_t* seq_ids, int32_t* ctx_lens,
@@ -981,6 +1048,35 @@ war_status war_profile_read(war_model* m, char* out, int32_t out_len) {
   m->prof.used = 0;
   m->prof.marks.clear();
   return (int64_t)text.size() < out_len ? WAR_OK : fail(WAR_ERR_INVALID_ARG, "profile text truncated");
+}
+
+war_status war_debug_sample(const float* logits, int32_t V, int32_t B, int32_t k_max, const int32_t* ntok,
+                            const int32_t* drafts, const float* uniforms, float temperature, int32_t top_k,
+                            int32_t* accept_lens, int32_t* next_tokens, void* stream) {
+  CHECK(logits && ntok && uniforms && next_tokens && (k_max == 0 || drafts), "null array");
+  CHECK(V >= 1 && B >= 1 && k_max >= 0, "bad sizes");
+  CHECK(std::isfinite(temperature) && temperature > 0.f, "temperature must be positive and finite");
+  CHECK(top_k >= 1 && top_k <= V, "top_k out of range [1, V]");
+  hipStream_t st = static_cast<hipStream_t>(stream);
+  DevBuf rows;
+  HIPCHK(rows.ensure((size_t)B * (k_max + 1) * 3 * 4));
+  SampleArgs sa{};
+  sa.logits = logits;
+  sa.V = V;
+  sa.ntok = ntok;
+  sa.drafts = drafts;
+  sa.k_max = k_max;
+  sa.kp1 = k_max + 1;
+  sa.B = B;
+  sa.uniforms = uniforms;
+  sa.temperature = temperature;
+  sa.top_k = top_k;
+  sa.row_out = rows.as<int32_t>();
+  launch_sample(sa, accept_lens, next_tokens, st);
+  const hipError_t e = hipStreamSynchronize(st);
+  rows.release();
+  HIPCHK(e);
+  return WAR_OK;
 }
 
 war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes) {

@@ -91,6 +91,11 @@ class DeviceStep:
         war.verify_step(model, pool, self.seq, self.ctx, self.last, self.drafts, self.dlens,
                         self.step.k_max, self.accept, self.next, self.logits if logits else None)
 
+    def verify_sampled(self, model: war.Model, pool: war.Pool, uniforms: torch.Tensor,
+                       temperature: float = 1.0, top_k: int = 200):
+        war.verify_step_sampled(model, pool, self.seq, self.ctx, self.last, self.drafts, self.dlens,
+                                self.step.k_max, uniforms, temperature, top_k, self.accept, self.next)
+
     def commit(self, pool: war.Pool, discard: bool = True):
         war.kv_commit(pool, self.seq, self.ctx, self.discard if discard else self.accept)
 

@@ -25,8 +25,8 @@ _ERRORS = {-1: "WAR_ERR_INVALID_ARG", -2: "WAR_ERR_OUT_OF_PAGES", -3: "WAR_ERR_H
 
 EXPORTS = ["war_weight_count", "war_model_create", "war_model_destroy", "war_kv_pool_create",
            "war_kv_pool_destroy", "war_kv_alloc", "war_kv_fork", "war_kv_free", "war_kv_load",
-           "war_prefill_append", "war_verify_step", "war_kv_commit", "war_pool_state",
-           "war_last_error", "war_debug_mfma16", "war_debug_workspace", "war_profile",
+           "war_prefill_append", "war_verify_step", "war_verify_step_sampled", "war_kv_commit", "war_pool_state",
+           "war_last_error", "war_debug_mfma16", "war_debug_workspace", "war_debug_sample", "war_profile",
            "war_profile_read"]
 
 
@@ -60,9 +60,12 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         "war_kv_load": (i32, [vp, i32, i32, i32, i32, vp, vp]),
         "war_prefill_append": (i32, [vp, vp, i32, vp, vp, pi32, vp, vp, vp, vp]),
         "war_verify_step": (i32, [vp, vp, i32, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp]),
+        "war_verify_step_sampled": (i32, [vp, vp, i32, vp, vp, vp, vp, vp, i32, vp, C.c_float, i32,
+                                          vp, vp, vp, vp]),
         "war_kv_commit": (i32, [vp, i32, vp, vp, vp, vp]),
         "war_pool_state": (i32, [vp, pi32, pi32, pi32, pi32, pi32, vp]),
         "war_last_error": (C.c_char_p, []),
+        "war_debug_sample": (i32, [vp, i32, i32, i32, vp, vp, vp, C.c_float, i32, vp, vp, vp]),
         "war_debug_mfma16": (i32, [vp, vp, vp, vp]),
         "war_debug_workspace": (i32, [vp, C.c_char_p, C.POINTER(vp), C.POINTER(C.c_int64)]),
         "war_profile": (i32, [vp, i32]),
@@ -219,6 +222,20 @@ def verify_step(model: Model, pool: Pool, seq_ids: torch.Tensor, ctx_lens: torch
                                  _ptr(accept_lens), _ptr(next_tokens), _ptr(logits), _stream(stream)))
 
 
+def verify_step_sampled(model: Model, pool: Pool, seq_ids: torch.Tensor, ctx_lens: torch.Tensor,
+                        last_tokens: torch.Tensor, draft_tokens: Optional[torch.Tensor],
+                        draft_lens: Optional[torch.Tensor], k_max: int, uniforms: torch.Tensor,
+                        temperature: float, top_k: int, accept_lens: torch.Tensor, next_tokens: torch.Tensor,
+                        logits: Optional[torch.Tensor] = None, stream=None) -> None:
+    """Sampled verification; uniforms fp32 [B * (k_max + 1), 2] on the device."""
+    assert uniforms.dtype == torch.float32 and uniforms.is_contiguous()
+    B = seq_ids.numel()
+    _check(lib().war_verify_step_sampled(model.handle, pool.handle, B, _ptr(seq_ids), _ptr(ctx_lens),
+                                         _ptr(last_tokens), _ptr(draft_tokens), _ptr(draft_lens), k_max,
+                                         _ptr(uniforms), float(temperature), int(top_k), _ptr(accept_lens),
+                                         _ptr(next_tokens), _ptr(logits), _stream(stream)))
+
+
 def kv_commit(pool: Pool, seq_ids: torch.Tensor, ctx_lens: torch.Tensor, accept_lens: torch.Tensor,
               stream=None) -> None:
     _check(lib().war_kv_commit(pool.handle, seq_ids.numel(), _ptr(seq_ids), _ptr(ctx_lens),
@@ -239,6 +256,16 @@ def debug_mfma16(A: torch.Tensor, B: torch.Tensor, stream=None) -> torch.Tensor:
     out = torch.empty((16, 16), dtype=torch.float32, device=A.device)
     _check(lib().war_debug_mfma16(_ptr(A.contiguous()), _ptr(B.contiguous()), _ptr(out), _stream(stream)))
     return out
+
+
+def debug_sample(logits: torch.Tensor, ntok: torch.Tensor, drafts: torch.Tensor, k_max: int,
+                 uniforms: torch.Tensor, temperature: float, top_k: int, accept_lens: torch.Tensor,
+                 next_tokens: torch.Tensor, stream=None) -> None:
+    """The sampled-verification decisions alone on given logit rows (war_debug.h)."""
+    B, V = ntok.numel(), logits.shape[-1]
+    _check(lib().war_debug_sample(_ptr(logits), V, B, k_max, _ptr(ntok), _ptr(drafts), _ptr(uniforms),
+                                  float(temperature), int(top_k), _ptr(accept_lens), _ptr(next_tokens),
+                                  _stream(stream)))
 
 
 def debug_workspace(model: Model, name: str, dtype: torch.dtype, shape) -> torch.Tensor:

@@ -11,6 +11,7 @@ import torch
 from oracle.accept import argmax_lowest
 from oracle.decoder import RequestKV, Weights
 from oracle.pages import PagePool
+from oracle.sampling import filtered_probs
 from oracle.verify import commit_request, greedy_decode, prefill_request, verify_request
 from paper_2607_17299_amd import synth
 from paper_2607_17299_amd.drafter import SuffixDrafter
@@ -384,6 +385,107 @@ def test_shared_prefix_cascade(tiny):
         np.testing.assert_allclose(g[0], K, atol=2e-2, rtol=2e-2)
         np.testing.assert_allclose(g[1], V, atol=2e-2, rtol=2e-2)
     print(f"\nshared-prefix cascade: reported {report}")
+
+
+def _near_decision(logits, T, top_k, err, margins):
+    """True if a logit error of `err` could change one of the sampled decisions
+    on the oracle's path: some margin (in probability) is below the bound
+    exp(2 err / T) - 1 on how far the error moves a probability or a cumulative
+    sum, plus twice the probability mass of the kept tokens within 2 err of the
+    top_k boundary (the kept set itself may change there)."""
+    delta = np.expm1(2 * err / T) + 1e-5
+    for i in range(len(margins)):
+        z = logits[min(i, len(logits) - 1)]
+        zs = np.sort(z)[::-1]
+        if top_k < z.size:
+            kth = zs[top_k - 1]
+            p = filtered_probs(z, T, top_k)
+            delta_i = delta + 2 * p[np.abs(z - kth) < 2 * err].sum()
+        else:
+            delta_i = delta
+        if margins[i] < delta_i:
+            return True
+    return False
+
+
+@pytest.mark.parametrize("T,top_k", [(1.0, 200), (0.7, 50)])
+def test_sampled_verification_matches_oracle(tiny, T, top_k):
+    """Three sampled verify steps (k = 4, ragged drafts: the oracle's greedy
+    continuation, partly corrupted) against the oracle's sampled rule on the
+    oracle's logits with the same uniforms.  With a nearly flat top-k target
+    the draw boundaries sit ~1e-3 apart, closer than the logit error can move
+    them, so many draws are legitimately near: a decision may differ only where
+    the logit error could move it (reported); both sides then continue from
+    the oracle's outcome.  The decision kernels themselves are checked exactly
+    in test_gpu_sampling.py."""
+    war, model, W = tiny["war"], tiny["model"], tiny["W"]
+    from oracle.sampling import verify_sampled
+    _, ctxs = _tiny_workload(seed=5, B=4, ctx_len=300)
+    B, k = len(ctxs), 4
+    pool, seq, ctx, kvs, onext, *_ = _prefill_both(tiny, ctxs)
+    rng = np.random.default_rng(21)
+    pending = [int(x) for x in onext]
+    report, checked = [], 0
+    t = lambda a: torch.as_tensor(np.asarray(a), dtype=torch.int32).to(DEV)
+    for step in range(3):
+        drafts = []
+        for b in range(B):
+            d = greedy_decode(CFG, W, copy.deepcopy(kvs[b]), pending[b], k)
+            d = [int(rng.integers(CFG.vocab)) if rng.random() < 0.25 else x for x in d]
+            drafts.append(d[: int(rng.integers(0, k + 1))])
+        dt = np.zeros((B, k), np.int32)
+        for b, d in enumerate(drafts):
+            dt[b, :len(d)] = d
+        u = rng.random((B * (k + 1), 2)).astype(np.float32)
+        acc, nx = t([0] * B), t([0] * B)
+        logits = torch.zeros((B * (k + 1), CFG.vocab), device=DEV)
+        war.verify_step_sampled(model, pool, seq, ctx, t(pending), t(dt), t([len(d) for d in drafts]), k,
+                                torch.from_numpy(u).to(DEV), T, top_k, acc, nx, logits)
+        torch.cuda.synchronize()
+        g_acc, g_nxt = acc.cpu().numpy(), nx.cpu().numpy()
+        glog = logits.cpu().numpy().reshape(B, k + 1, CFG.vocab)
+        o_acc = []
+        for b in range(B):
+            n = len(drafts[b])
+            r = verify_request(CFG, W, kvs[b], pending[b], drafts[b])
+            uu = u[b * (k + 1): b * (k + 1) + n + 1].astype(np.float64)
+            rs = verify_sampled(r["logits"], drafts[b], uu[:, 0], uu[:, 1], T, top_k)
+            err = float(np.abs(glog[b, : n + 1] - r["logits"]).max())
+            assert err < 5e-2, err
+            if (int(g_acc[b]), int(g_nxt[b])) != (rs["accept"], rs["next"]):
+                assert _near_decision(r["logits"], T, top_k, err, rs["margins"]), \
+                    (step, b, (int(g_acc[b]), int(g_nxt[b])), (rs["accept"], rs["next"]), rs["margins"], err)
+                report.append(f"step {step} req {b}: near-boundary sample differs")
+            else:
+                checked += 1
+            commit_request(kvs[b], r, rs["accept"])
+            pending[b] = rs["next"]
+            o_acc.append(rs["accept"])
+        war.kv_commit(pool, seq, ctx, t(o_acc))
+        torch.cuda.synchronize()
+        assert ctx.cpu().tolist() == [kv.length for kv in kvs]
+    print(f"\nsampled T={T} top_k={top_k}: {checked} exact, reported {report}")
+
+
+def test_sampled_top1_equals_greedy(tiny):
+    """top_k = 1 makes every target a point mass on the argmax: the sampled
+    step must reproduce the greedy step exactly, for any uniforms."""
+    war, model = tiny["war"], tiny["model"]
+    _, ctxs = _tiny_workload(seed=6, B=4, ctx_len=200)
+    B, k = len(ctxs), 4
+    pool, seq, ctx, kvs, onext, *_ = _prefill_both(tiny, ctxs)
+    rng = np.random.default_rng(22)
+    t = lambda a: torch.as_tensor(np.asarray(a), dtype=torch.int32).to(DEV)
+    dt = rng.integers(0, CFG.vocab, (B, k)).astype(np.int32)
+    dl = [0, 2, 4, 3]
+    ga, gn, sa, sn = t([0] * B), t([0] * B), t([0] * B), t([0] * B)
+    war.verify_step(model, pool, seq, ctx, t(onext), t(dt), t(dl), k, ga, gn)
+    war.kv_commit(pool, seq, ctx, t([-1] * B))
+    u = torch.from_numpy(rng.random((B * (k + 1), 2)).astype(np.float32)).to(DEV)
+    war.verify_step_sampled(model, pool, seq, ctx, t(onext), t(dt), t(dl), k, u, 1.0, 1, sa, sn)
+    war.kv_commit(pool, seq, ctx, t([-1] * B))
+    torch.cuda.synchronize()
+    assert sa.cpu().tolist() == ga.cpu().tolist() and sn.cpu().tolist() == gn.cpu().tolist()
 
 
 @pytest.mark.parametrize("mode", ["suffix", "greedy", "mixed"])
