@@ -16,6 +16,17 @@ next_b is the argmax of the last row.
 
 Requests are processed one at a time, so a request's result never depends on
 what else is in the batch.
+
+Tree drafts (SuffixDecoding proposes speculation trees; the paper names their
+tree-mask handling as a verification cost: Evaluation): node 0 is x_b, node j
+(1..n) carries draft token d_j and a parent in 0..j-1.  Node j is scored by
+the decoder on its own root-to-node path (the plain definition: exactly what
+token-by-token decode along that path computes).  A node is accepted when its
+parent is (the root always is) and its token equals the parent's greedy token;
+the accepted path ends at the deepest accepted node (ties: the lowest node
+index), a_b is its depth and next_b its greedy token.  Without two siblings
+carrying the same token this is the walk from the root that follows the one
+matching child.  The committed KV is that of the accepted path.
 """
 from __future__ import annotations
 
@@ -34,6 +45,38 @@ def verify_request(cfg, W: Weights, kv: RequestKV, last_token: int, drafts: Sequ
     g = argmax_lowest(logits)
     a = accept_length(drafts, g)
     return {"logits": logits, "greedy": g, "accept": a, "next": int(g[a]), "new_kv": new_kv}
+
+
+def tree_path(parents: Sequence[int], j: int) -> List[int]:
+    """Node indices from the root (0) to node j; parents[i-1] is node i's parent."""
+    path = [j]
+    while path[-1] != 0:
+        path.append(int(parents[path[-1] - 1]))
+    return path[::-1]
+
+
+def verify_tree_request(cfg, W: Weights, kv: RequestKV, last_token: int, drafts: Sequence[int],
+                        parents: Sequence[int], rounding: bool = True) -> Dict:
+    n = len(drafts)
+    assert len(parents) == n and all(0 <= int(parents[i]) <= i for i in range(n))
+    tok = [int(last_token)] + [int(d) for d in drafts]
+    rows = []
+    for j in range(n + 1):
+        lg, _ = forward_block(cfg, W, [tok[i] for i in tree_path(parents, j)], kv.length, kv.get, rounding)
+        rows.append(lg[-1])
+    logits = np.stack(rows)
+    g = argmax_lowest(logits)
+    # a node is accepted when its parent is and its token is the parent's greedy token
+    ok, depth = [True] + [False] * n, [0] * (n + 1)
+    for j in range(1, n + 1):
+        p = int(parents[j - 1])
+        ok[j] = ok[p] and tok[j] == int(g[p])
+        depth[j] = depth[p] + 1
+    cur = max((j for j in range(n + 1) if ok[j]), key=lambda j: (depth[j], -j))
+    path = tree_path(parents, cur)[1:]
+    _, new_kv = forward_block(cfg, W, [tok[i] for i in [0] + path], kv.length, kv.get, rounding)
+    return {"logits": logits, "greedy": g, "accept": len(path), "path": path, "next": int(g[cur]),
+            "new_kv": new_kv}
 
 
 def verify_batch(cfg, W: Weights, kvs: List[RequestKV], last_tokens, drafts: List[Sequence[int]],
