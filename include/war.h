@@ -195,6 +195,31 @@ war_status war_verify_step_sampled(war_model* m, war_kv_pool* p, int32_t B, cons
                                    const float* uniforms, float temperature, int32_t top_k,
                                    int32_t* accept_lens, int32_t* next_tokens, float* logits, void* stream);
 
+/* The verify step with a draft TREE per request (SuffixDecoding proposes
+ * speculation trees; the paper counts their tree-mask handling among the
+ * verification costs: Evaluation).  Greedy acceptance.  Same arguments and
+ * pool protocol as war_verify_step, plus:
+ *   draft_parents device int32 [B][k_max]: node 0 is last_token, node i
+ *                 (1..draft_len) carries draft_tokens[b][i-1] and has parent
+ *                 draft_parents[b][i-1] in [0, i).  A parent outside that range
+ *                 sets the device error flag (war_pool_state) and is read as i-1.
+ *   accept_path   device int32 [B][k_max] out, or NULL: the accepted nodes in
+ *                 depth order, -1 beyond accept_lens[b].
+ *   k_max         + 1 <= 32.
+ * Node i is scored on its root-to-node path: position ctx + depth(i), and it
+ * sees the cached context and the nodes of that path.  Its logits are row
+ * b*(k_max+1)+i.  A node is accepted when its parent is (the root always is)
+ * and its token is the parent's greedy token; the accepted path ends at the
+ * deepest accepted node (lowest index among equals), accept_lens[b] is its
+ * depth and next_tokens[b] its greedy token.  Before returning, the step moves
+ * the KV of the accepted nodes to slots ctx + 1 .. ctx + accept_lens[b], so
+ * war_kv_commit keeps exactly the accepted path. */
+war_status war_verify_step_tree(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                                const int32_t* ctx_lens, const int32_t* last_tokens,
+                                const int32_t* draft_tokens, const int32_t* draft_parents,
+                                const int32_t* draft_lens, int32_t k_max, int32_t* accept_lens,
+                                int32_t* next_tokens, int32_t* accept_path, float* logits, void* stream);
+
 /* Commit the pending verify step.
  *   accept_lens device int32 [B]; -1 discards the step.  Values are clamped
  *               to [-1, reserved capacity].
@@ -213,7 +238,8 @@ war_status war_kv_commit(war_kv_pool* p, int32_t B, const int32_t* seq_ids, int3
  *   held            [max_seqs]   pages held per sequence
  *   step_base       [max_seqs]   pages held before the last reservation
  * Returns WAR_ERR_DEVICE if a kernel flagged bad device-side input (a token
- * id outside [0, vocab), or a device page shortage). */
+ * id outside [0, vocab), a tree parent out of range, or a device page
+ * shortage). */
 war_status war_pool_state(war_kv_pool* p, int32_t* free_count, int32_t* free_stack,
                           int32_t* refcount, int32_t* held, int32_t* step_base, void* stream);
 

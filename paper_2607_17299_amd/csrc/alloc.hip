@@ -101,7 +101,8 @@ __global__ void __launch_bounds__(kBT) k_grow(PoolDev p, int n, const int32_t* s
 
 // Verify-step setup: reserve pages for ctx + draft_len + 1 slots per request,
 // then build the padded row layout (row b*(k+1)+i = request b, token i) and the
-// attention work list (one item per `chunk` keys of each request).
+// attention work list (one item per `chunk` keys of each request).  With tree
+// drafts (k_max + 1 <= 32) token i is tree node i.
 __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs a, StepMeta m) {
   __shared__ int sh[16];
   __shared__ int s_fail;
@@ -259,7 +260,29 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
     m.tok[r] = tok;
     m.active[r] = act ? 1 : 0;
     m.row_req[r] = b;
-    m.pos[r] = s_ctx[b] + min(i, max(dlb, 0));
+    const int slot = s_ctx[b] + min(i, max(dlb, 0));
+    if (a.draft_parents) {
+      // tree drafts: node i sits in slot ctx + i at position ctx + depth; its
+      // mask holds the nodes of its root path.  A parent outside [0, i) is
+      // flagged and read as i - 1, so the walk always ends.
+      int depth = 0;
+      uint32_t msk = 1u;
+      if (act)
+        for (int j = i; j > 0; ++depth) {
+          msk |= 1u << j;
+          int pj = a.draft_parents[(int64_t)b * a.k_max + j - 1];
+          if (pj < 0 || pj >= j) {
+            atomicOr(&p.scalars[1], ERR_BAD_PARENT);
+            pj = j - 1;
+          }
+          j = pj;
+        }
+      m.pos[r] = s_ctx[b] + depth;
+      m.kvpos[r] = slot;
+      m.tmask[r] = msk;
+    } else {
+      m.pos[r] = slot;
+    }
   }
 }
 

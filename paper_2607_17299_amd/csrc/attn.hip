@@ -1,7 +1,8 @@
 // Grouped-query verification attention over the paged KV cache (gfx950).
 //
 // Row r of a (request, kv-head) block is token t0 + r / G of that request for
-// query head kvh*G + r % G; it sees keys 0 .. pos(row).  A verify step has
+// query head kvh*G + r % G; it sees keys 0 .. pos(row) (tree drafts: the context
+// and the step slots of its node's root path).  A verify step has
 // G*(draft_len+1) such rows per request and kv-head (4..48); the keys number
 // tens of thousands, so the kernel is bound by reading K and V from HBM once.
 //
@@ -42,7 +43,8 @@ struct KVFrag {
 // QLDS = queries read from LDS instead of registers; WPE = waves per SIMD the
 // register budget allows.  Two waves per SIMD let one wave's MFMA/softmax work
 // overlap the other's memory waits.
-template <int NR, int HD, int DEPTH, bool QLDS, int WPE>
+// TREE = the step has tree drafts (rows carry node masks).
+template <int NR, int HD, int DEPTH, bool QLDS, int WPE, bool TREE>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 k_attn(AttnArgs a) {
   constexpr int DPL = HD / 4;    // dims per lane group in the S^T operands
@@ -54,6 +56,7 @@ k_attn(AttnArgs a) {
   __shared__ float s_m[4][RB], s_l[4][RB];
   __shared__ float s_o[RB * OST];
   __shared__ __attribute__((aligned(16))) bf16_t s_q[QLDS ? RB * QST : 8];
+  __shared__ uint32_t s_tm[TREE ? RB : 1];  // tree drafts: step slots each row sees
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
   const int total = (a.meta.order ? a.meta.n_items[1] : a.meta.n_items[0]) * a.n_kv_heads;
   const int P = a.kv.page_size;
@@ -81,6 +84,23 @@ k_attn(AttnArgs a) {
       for (int jm = 1; jm < nmem; ++jm) nrows += min(a.TB, a.meta.req_ntok[b + jm]) * a.G;
     const int last_pos = shared ? (chunk + 1) * a.chunk - 1 : pos0 + t0 + nt - 1;
     const int qpos0 = shared ? last_pos + 1 : pos0 + t0;  // smallest row position
+    // tree drafts: every key at or past the context needs its row's node mask
+    // (a shared-prefix unit's keys all precede the context)
+    const int mask_from = TREE ? pos0 - 1 : qpos0;
+    if constexpr (TREE) {
+      // the node mask relative to the row's own slot: bit d = slot rpos - d is
+      // visible (bits past the node index: context keys, always visible)
+      if (tid < RB) {
+        uint32_t rm = 0xffffffffu;
+        if (!shared && tid < nrows) {
+          const int i = t0 + tid / a.G;
+          rm = __brev(a.meta.tmask[row0 + i]) >> (31 - i);
+          if (i < 31) rm |= 0xffffffffu << (i + 1);
+        }
+        s_tm[tid] = rm;
+      }
+      __syncthreads();
+    }
     const int S = last_pos + 1;
     const int kbeg = chunk * a.chunk, kend = min(S, kbeg + a.chunk);
     // row r -> (query row, query head) and its partial row; false if r is not live
@@ -184,7 +204,7 @@ k_attn(AttnArgs a) {
 
     auto compute_block = [&](const KVFrag<HD>& f, int kb) {
       // keys of this block above the smallest row position need the causal mask
-      const bool tail = kb + 31 > qpos0;
+      const bool tail = kb + 31 > mask_from;
       if constexpr (QLDS) asm volatile("" ::: "memory");  // re-read Q from LDS each block
       // phase 1: scores of every row tile (the K fragments die after this)
       float sc[NR][8];
@@ -209,9 +229,19 @@ k_attn(AttnArgs a) {
       for (int rt = 0; rt < NR; ++rt) {
         float* sv = sc[rt];
         if (tail) {
+          if constexpr (TREE) {
+            // a tree row sees the step slot pos0 + i only when node i is on its path
+            const uint32_t tm = s_tm[rt * 16 + ln];
 #pragma unroll
-          for (int e = 0; e < 8; ++e)
-            if (kb + lg * 8 + e > rpos[rt]) sv[e] = -INFINITY;
+            for (int e = 0; e < 8; ++e) {
+              const int dd = rpos[rt] - (kb + lg * 8 + e);
+              if (dd < 0 || !((tm >> min(dd, 31)) & 1u)) sv[e] = -INFINITY;
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 8; ++e)
+              if (kb + lg * 8 + e > rpos[rt]) sv[e] = -INFINITY;
+          }
         }
         float lm = sv[0];
 #pragma unroll
@@ -421,10 +451,18 @@ template <int NR>
 void launch_attn_nr(const AttnArgs& a, int head_dim, int grid, hipStream_t st) {
   constexpr int DEPTH = NR == 1 ? 1 : 0;
   constexpr bool QLDS = NR > 1;
-  if (head_dim == 128)
-    k_attn<NR, 128, DEPTH, QLDS, 2><<<grid, 256, 0, st>>>(a);
-  else
-    k_attn<NR, 64, DEPTH, QLDS, 2><<<grid, 256, 0, st>>>(a);
+  const bool tree = a.meta.tmask != nullptr;
+  if (head_dim == 128) {
+    if (tree)
+      k_attn<NR, 128, DEPTH, QLDS, 2, true><<<grid, 256, 0, st>>>(a);
+    else
+      k_attn<NR, 128, DEPTH, QLDS, 2, false><<<grid, 256, 0, st>>>(a);
+  } else {
+    if (tree)
+      k_attn<NR, 64, DEPTH, QLDS, 2, true><<<grid, 256, 0, st>>>(a);
+    else
+      k_attn<NR, 64, DEPTH, QLDS, 2, false><<<grid, 256, 0, st>>>(a);
+  }
 }
 
 template <int RB>

@@ -97,6 +97,11 @@ struct StepMeta {
   int32_t* seg_count;   // [n_segs]
   int32_t* seg_req;     // [n_segs]
   int32_t* seg_rb;      // [n_segs]
+  // Tree drafts (both null otherwise): the KV slot of each row (its node index
+  // past the context, while pos is the context plus the node's depth) and the
+  // step slots the row sees, bit i = node i (its root-to-node path).
+  int32_t* kvpos;
+  uint32_t* tmask;
 };
 
-enum { ERR_BAD_TOKEN = 1, ERR_NO_PAGES = 2 };
+enum { ERR_BAD_TOKEN = 1, ERR_NO_PAGES = 2, ERR_BAD_PARENT = 4 };

@@ -29,6 +29,7 @@ struct VerifySetupArgs {
   const int32_t* last_tokens;
   const int32_t* draft_tokens;
   const int32_t* draft_lens;
+  const int32_t* draft_parents;  // nullable: tree drafts [B][k_max], parent of node i+1
 };
 
 // C[m][n] = sum_k A[arow(m)][k] * W[n][k]   (bf16 in, fp32 accumulate)
@@ -123,6 +124,14 @@ void launch_qkv_rope(int rows, int splits, const float* P, const ModelDims& md,
                      const int32_t* row_req, const int32_t* table, int max_pages, const KvGeom& kv,
                      int layer, bf16_t* q, hipStream_t st);
 void launch_swiglu(int rows, int splits, const float* P, int F, bf16_t* y, hipStream_t st);
+// parents (nullable): tree drafts; accept_path [n_req][k_max] then receives the
+// accepted nodes in depth order, -1 beyond the accept length
 void launch_argmax_accept(int n_req, const int32_t* ntok, int row_stride, int n_blocks,
                           const float* amax_v, const int32_t* amax_i, const int32_t* draft_tokens,
-                          int k_max, int32_t* accept_lens, int32_t* next_tokens, hipStream_t st);
+                          const int32_t* parents, int k_max, int32_t* accept_lens, int32_t* next_tokens,
+                          int32_t* accept_path, hipStream_t st);
+// Tree drafts: move the KV of each request's accepted nodes (slots ctx + node)
+// to slots ctx + 1 .. ctx + accept_len, every layer.
+void launch_kv_compact(const KvGeom& kv, int n_layers, int B, const StepMeta& meta, const int32_t* table,
+                       int max_pages, const int32_t* accept_lens, const int32_t* accept_path, int k_max,
+                       hipStream_t st);

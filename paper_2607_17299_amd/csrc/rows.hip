@@ -99,7 +99,7 @@ __global__ void __launch_bounds__(1024) k_residual_norm(int rows, int splits, co
 
 // Sum the QKV partials of one row, rotate q and k (rotate-half pairs (j, j+D/2)),
 // round to bf16; q goes to its buffer, k and v of active rows into the KV page slot
-// of the row's position.
+// of the row's position (a tree node's own slot, when the step has tree drafts).
 __global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const float* P, ModelDims md,
                                                   const float* cos_t, const float* sin_t,
                                                   StepMeta meta, const int32_t* row_req,
@@ -114,7 +114,7 @@ __global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const fl
   if (p >= n_pairs) return;
   int page = 0, slot = 0;
   if (act) {
-    const int pos = meta.pos[r];
+    const int pos = meta.kvpos ? meta.kvpos[r] : meta.pos[r];
     const int seq = meta.req_seq[row_req[r]];
     page = table[(int64_t)seq * max_pages + pos / kv.page_size];
     slot = pos % kv.page_size;
@@ -188,15 +188,20 @@ __global__ void __launch_bounds__(256) k_swiglu(int rows, int splits, const floa
 }
 
 // Per request: greedy token of each active row (best over the LM head's column
-// blocks, ties -> lowest id), then the longest draft prefix that matches.
+// blocks, ties -> lowest id), then the acceptance.  Chain drafts: the longest
+// draft prefix that matches.  Tree drafts: a node is accepted when its parent
+// is and its token is the parent's greedy token; the deepest accepted node
+// (lowest index among equals) ends the accepted path.
 __global__ void __launch_bounds__(256) k_argmax_accept(const int32_t* ntok, int row_stride,
                                                        int n_blocks, const float* amax_v,
                                                        const int32_t* amax_i,
-                                                       const int32_t* drafts, int k_max,
-                                                       int32_t* accept_lens, int32_t* next_tokens) {
+                                                       const int32_t* drafts, const int32_t* parents,
+                                                       int k_max, int32_t* accept_lens, int32_t* next_tokens,
+                                                       int32_t* accept_path) {
   __shared__ float sv[4];
   __shared__ int si[4];
   __shared__ int greedy[64];
+  __shared__ int s_par[64], s_dep[64], s_ok[64];
   const int b = blockIdx.x;
   const int n = ntok ? min(ntok[b], 64) : 1;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
@@ -236,13 +241,68 @@ __global__ void __launch_bounds__(256) k_argmax_accept(const int32_t* ntok, int 
     }
     __syncthreads();
   }
-  if (threadIdx.x == 0) {
-    int a = 0;
-    if (n > 0) {
-      while (a < n - 1 && drafts && drafts[(int64_t)b * k_max + a] == greedy[a]) ++a;
+  if (threadIdx.x != 0) return;
+  int a = 0, last = 0;
+  if (parents && n > 0) {
+    s_ok[0] = 1;
+    s_dep[0] = 0;
+    for (int j = 1; j < n; ++j) {
+      int pj = parents[(int64_t)b * k_max + j - 1];
+      if (pj < 0 || pj >= j) pj = j - 1;  // flagged by the step setup
+      s_par[j] = pj;
+      s_dep[j] = s_dep[pj] + 1;
+      s_ok[j] = s_ok[pj] && drafts[(int64_t)b * k_max + j - 1] == greedy[pj];
+      if (s_ok[j] && s_dep[j] > s_dep[last]) last = j;
     }
-    if (accept_lens) accept_lens[b] = a;
-    next_tokens[b] = n > 0 ? greedy[a] : -1;
+    a = s_dep[last];
+    for (int d = a; d < k_max; ++d) accept_path[(int64_t)b * k_max + d] = -1;
+    for (int j = last; j > 0; j = s_par[j]) accept_path[(int64_t)b * k_max + s_dep[j] - 1] = j;
+  } else if (n > 0) {
+    while (a < n - 1 && drafts && drafts[(int64_t)b * k_max + a] == greedy[a]) ++a;
+    last = a;
+  } else if (parents) {
+    for (int d = 0; d < k_max; ++d) accept_path[(int64_t)b * k_max + d] = -1;
+  }
+  if (accept_lens) accept_lens[b] = a;
+  next_tokens[b] = n > 0 ? greedy[last] : -1;
+}
+
+// Tree drafts: one workgroup per (layer, kv-head, request) gathers the K rows and
+// V^T columns of the accepted nodes into LDS, then writes them to slots
+// ctx + 1 .. ctx + a (node d of the path has index >= d, so a sequential copy
+// in depth order would also be safe; staging makes the order irrelevant).
+constexpr int kCompactMaxNodes = 31, kCompactMaxDim = 128;
+__global__ void __launch_bounds__(256) k_kv_compact(KvGeom kv, StepMeta meta, const int32_t* table,
+                                                    int max_pages, const int32_t* accept_lens,
+                                                    const int32_t* accept_path, int k_max) {
+  __shared__ bf16_t s_k[kCompactMaxNodes][kCompactMaxDim], s_v[kCompactMaxNodes][kCompactMaxDim];
+  __shared__ int s_src[kCompactMaxNodes];
+  const int layer = blockIdx.x, kvh = blockIdx.y, b = blockIdx.z;
+  const int n = meta.req_ntok[b];
+  const int a = min(min(accept_lens[b], n - 1), k_max);
+  if (a <= 0) return;
+  const int D = kv.head_dim, P = kv.page_size;
+  const int ctx = meta.req_pos0[b];
+  const int32_t* trow = table + (int64_t)meta.req_seq[b] * max_pages;
+  if (threadIdx.x < a) {
+    const int src = accept_path[(int64_t)b * k_max + threadIdx.x];
+    s_src[threadIdx.x] = (src >= 1 && src < n) ? src : threadIdx.x + 1;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < a * D; e += blockDim.x) {
+    const int d = e / D, c = e % D;
+    const int sp = ctx + s_src[d];
+    const int pg = trow[sp / P], sl = sp % P;
+    s_k[d][c] = kv.kv[kv.page_elems(layer, pg, kvh, 0) + (int64_t)sl * D + c];
+    s_v[d][c] = kv.kv[kv.page_elems(layer, pg, kvh, 1) + (int64_t)c * P + sl];
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < a * D; e += blockDim.x) {
+    const int d = e / D, c = e % D;
+    const int dp = ctx + d + 1;
+    const int pg = trow[dp / P], sl = dp % P;
+    kv.kv[kv.page_elems(layer, pg, kvh, 0) + (int64_t)sl * D + c] = s_k[d][c];
+    kv.kv[kv.page_elems(layer, pg, kvh, 1) + (int64_t)c * P + sl] = s_v[d][c];
   }
 }
 
@@ -274,7 +334,14 @@ void launch_swiglu(int rows, int splits, const float* P, int F, bf16_t* y, hipSt
 }
 void launch_argmax_accept(int n_req, const int32_t* ntok, int row_stride, int n_blocks,
                           const float* amax_v, const int32_t* amax_i, const int32_t* draft_tokens,
-                          int k_max, int32_t* accept_lens, int32_t* next_tokens, hipStream_t st) {
+                          const int32_t* parents, int k_max, int32_t* accept_lens, int32_t* next_tokens,
+                          int32_t* accept_path, hipStream_t st) {
   k_argmax_accept<<<n_req, 256, 0, st>>>(ntok, row_stride, n_blocks, amax_v, amax_i, draft_tokens,
-                                         k_max, accept_lens, next_tokens);
+                                         parents, k_max, accept_lens, next_tokens, accept_path);
+}
+void launch_kv_compact(const KvGeom& kv, int n_layers, int B, const StepMeta& meta, const int32_t* table,
+                       int max_pages, const int32_t* accept_lens, const int32_t* accept_path, int k_max,
+                       hipStream_t st) {
+  dim3 grid(n_layers, kv.n_kv_heads, B);
+  k_kv_compact<<<grid, 256, 0, st>>>(kv, meta, table, max_pages, accept_lens, accept_path, k_max);
 }

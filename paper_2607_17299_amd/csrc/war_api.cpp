@@ -107,6 +107,9 @@ struct war_model {
   DevBuf segs_i32;  // begin, count, req, rb      [4][n_seg_cap]
   DevBuf n_items, items, order, pm, pl, po, a_rows;
   DevBuf logits_ws, row_out;  // sampled verification: full logits, per-row outcomes
+  DevBuf tree_i32;            // tree drafts: kvpos, tmask [2][max_rows]
+  DevBuf path_ws;             // tree drafts: accepted path when the caller passes none
+  bool tree_step = false;     // the metadata describes tree drafts
   int n_req_cap, n_seg_cap;
   std::vector<int32_t> h_stage;  // host staging for prefill metadata
   DevBuf stage_dev;              // device copy of per-prefill host arrays
@@ -134,6 +137,9 @@ struct war_model {
     m.seg_count = s4 + n_seg_cap;
     m.seg_req = s4 + 2 * n_seg_cap;
     m.seg_rb = s4 + 3 * n_seg_cap;
+    int32_t* t2 = tree_i32.as<int32_t>();
+    m.kvpos = tree_step ? t2 : nullptr;
+    m.tmask = tree_step ? reinterpret_cast<uint32_t*>(t2 + max_rows) : nullptr;
     return m;
   }
 };
@@ -498,6 +504,7 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
   ok(m->amax_v.ensure((size_t)R * (md.V / 128) * 4));
   ok(m->amax_i.ensure((size_t)R * (md.V / 128) * 4));
   ok(m->rows_i32.ensure((size_t)4 * R * 4));
+  ok(m->tree_i32.ensure((size_t)2 * R * 4));
   ok(m->reqs_i32.ensure((size_t)4 * m->n_req_cap * 4));
   ok(m->segs_i32.ensure((size_t)4 * m->n_seg_cap * 4));
   ok(m->n_items.ensure(16));
@@ -518,7 +525,7 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
 void war_model_destroy(war_model* m) {
   if (!m) return;
   for (DevBuf* b : {&m->wts, &m->h, &m->u, &m->q, &m->o, &m->y, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
-                    &m->amax_v, &m->amax_i, &m->rows_i32, &m->reqs_i32, &m->segs_i32, &m->n_items,
+                    &m->amax_v, &m->amax_i, &m->rows_i32, &m->tree_i32, &m->path_ws, &m->reqs_i32, &m->segs_i32, &m->n_items,
                     &m->items, &m->order, &m->logits_ws, &m->row_out, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
     b->release();
   if (m->pinned) (void)hipHostFree(m->pinned);
@@ -593,7 +600,10 @@ war_status war_pool_state(war_kv_pool* p, int32_t* free_count, int32_t* free_sta
   if (refcount) HIPCHK(hipMemcpy(refcount, p->dev.refcount, (size_t)p->dev.num_pages * 4, hipMemcpyDeviceToHost));
   if (held) HIPCHK(hipMemcpy(held, p->dev.held, (size_t)p->dev.max_seqs * 4, hipMemcpyDeviceToHost));
   if (step_base) HIPCHK(hipMemcpy(step_base, p->dev.base, (size_t)p->dev.max_seqs * 4, hipMemcpyDeviceToHost));
-  if (err) return fail(WAR_ERR_DEVICE, err & ERR_NO_PAGES ? "device page shortage" : "bad token id or context length on device");
+  if (err)
+    return fail(WAR_ERR_DEVICE, err & ERR_NO_PAGES     ? "device page shortage"
+                                : err & ERR_BAD_PARENT ? "tree parent out of range on device"
+                                                       : "bad token id or context length on device");
   return WAR_OK;
 }
 
@@ -704,7 +714,8 @@ struct SampleParams {
 war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
                        const int32_t* ctx_lens, const int32_t* last_tokens, const int32_t* draft_tokens,
                        const int32_t* draft_lens, int32_t k_max, int32_t* accept_lens,
-                       int32_t* next_tokens, float* logits, void* stream, const SampleParams& sp) {
+                       int32_t* next_tokens, float* logits, void* stream, const SampleParams& sp,
+                       const int32_t* draft_parents = nullptr, int32_t* accept_path = nullptr) {
   CHECK(m && p, "null model or pool");
   CHECK(same_shape(m->cfg, p->cfg), "model and pool shapes differ");
   CHECK(!p->pending, "previous verify step not committed");
@@ -717,6 +728,9 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
   CHECK(k_max == 0 || draft_tokens, "draft_tokens required when k_max > 0");
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int P = p->dev.page_size;
+  const bool tree = draft_parents != nullptr && k_max > 0;
+  if (tree && k_max + 1 > 32) return fail(WAR_ERR_UNSUPPORTED, "tree drafts: k_max + 1 must be <= 32");
+  if (tree && sp.uniforms) return fail(WAR_ERR_UNSUPPORTED, "tree drafts are verified greedily");
 
   // capacity: ctx + draft + 1 slots need at most cdiv(k_max+1, P) new pages per request
   const int64_t bound = (int64_t)B * cdiv_i(k_max + 1, P);
@@ -764,6 +778,12 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
   va.G = G;
   va.rb = RB;
   va.cascade = p->forked && B > 1 ? 1 : 0;  // shared-prefix units for forked siblings
+  va.draft_parents = tree ? draft_parents : nullptr;
+  m->tree_step = tree;
+  if (tree && !accept_path) {
+    HIPCHK(m->path_ws.ensure((size_t)B * k_max * 4));
+    accept_path = m->path_ws.as<int32_t>();
+  }
   {
     Timed t(m->prof, st, "verify_setup");
     launch_verify_setup(p->dev, va, m->meta(), st);
@@ -810,7 +830,13 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
     }
     Timed t(m->prof, st, "argmax_accept");
     launch_argmax_accept(B, m->meta().req_ntok, kp1, m->md.V / 128, m->amax_v.as<float>(),
-                         m->amax_i.as<int32_t>(), draft_tokens, k_max, accept_lens, next_tokens, st);
+                         m->amax_i.as<int32_t>(), draft_tokens, tree ? draft_parents : nullptr, k_max,
+                         accept_lens, next_tokens, accept_path, st);
+  }
+  if (tree) {
+    Timed t(m->prof, st, "kv_compact");
+    launch_kv_compact(p->geom, m->cfg.n_layers, B, m->meta(), p->dev.table, p->dev.max_pages, accept_lens,
+                      accept_path, k_max, st);
   }
   HIPCHK(hipGetLastError());
   p->free_lb -= need;
@@ -848,6 +874,16 @@ war_status war_verify_step_sampled(war_model* m, war_kv_pool* p, int32_t B, cons
                      next_tokens, logits, stream, sp);
 }
 
+war_status war_verify_step_tree(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                                const int32_t* ctx_lens, const int32_t* last_tokens,
+                                const int32_t* draft_tokens, const int32_t* draft_parents,
+                                const int32_t* draft_lens, int32_t k_max, int32_t* accept_lens,
+                                int32_t* next_tokens, int32_t* accept_path, float* logits, void* stream) {
+  CHECK(k_max == 0 || draft_parents, "draft_parents required when k_max > 0");
+  return verify_impl(m, p, B, seq_ids, ctx_lens, last_tokens, draft_tokens, draft_lens, k_max, accept_lens,
+                     next_tokens, logits, stream, SampleParams{}, draft_parents, accept_path);
+}
+
 war_status war_kv_commit(war_kv_pool* p, int32_t B, const int32_t* seq_ids, int32_t* ctx_lens,
                          const int32_t* accept_lens, void* stream) {
   CHECK(p, "null pool");
@@ -871,6 +907,7 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int P = p->dev.page_size;
   const int G = m->md.nq / m->md.nkv;
+  m->tree_step = false;  // prefill rows are a causal chain
   int64_t total = 0;
   for (int i = 0; i < n; ++i) {
     CHECK(n_new_host[i] >= 1, "n_new must be >= 1");
@@ -1002,7 +1039,7 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
       gemm(m, m->u.as<bf16_t>(), m->md.d, m->a_rows.as<int32_t>(), m->w_lm, nl, m->md.V,
            m->md.d, &sd, st, true, last_logits ? last_logits + (int64_t)first_seq * m->md.V : nullptr);
       launch_argmax_accept(nl, nullptr, 1, m->md.V / 128, m->amax_v.as<float>(), m->amax_i.as<int32_t>(),
-                           nullptr, 0, nullptr, next_tokens + first_seq, st);
+                           nullptr, nullptr, 0, nullptr, next_tokens + first_seq, nullptr, st);
       HIPCHK(hipGetLastError());
       HIPCHK(hipStreamSynchronize(st));  // last_rows goes out of scope
     }
@@ -1085,7 +1122,8 @@ war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64
   const DevBuf* b = n == "h" ? &m->h : n == "u" ? &m->u : n == "q" ? &m->q : n == "o" ? &m->o
                   : n == "P" ? &m->P : n == "pm" ? &m->pm : n == "pl" ? &m->pl : n == "po" ? &m->po
                   : n == "rows" ? &m->rows_i32 : n == "reqs" ? &m->reqs_i32 : n == "items" ? &m->items
-                  : n == "order" ? &m->order : n == "n_items" ? &m->n_items : nullptr;
+                  : n == "order" ? &m->order : n == "n_items" ? &m->n_items
+                  : n == "tree" ? &m->tree_i32 : nullptr;
   CHECK(b, "unknown workspace buffer");
   *ptr = b->p;
   *bytes = (int64_t)b->bytes;

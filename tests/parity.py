@@ -73,3 +73,49 @@ def shared_units(rows, rb):
         cur += r
         n += 1
     return runs + [n]
+
+
+def tree_path_brute(tokens, parents, greedy):
+    """Accepted path of a draft tree by enumerating every root-to-node path:
+    the longest whose every node carries its parent's greedy token, the lowest
+    end node among equally long ones.  tokens[0] is the root's token."""
+    best = []
+    for j in range(len(tokens)):
+        path, c = [], j
+        while c != 0:
+            path.append(c)
+            c = parents[c - 1]
+        path = path[::-1]
+        prev = [0] + path
+        if all(tokens[c] == greedy[prev[k]] for k, c in enumerate(path)) and len(path) > len(best):
+            best = path
+    return best
+
+
+def compare_tree_request(o: Dict, g_logits: np.ndarray, tokens, parents, g_accept: int, g_next: int,
+                         g_path, report: List[str], tag: str, tol: float = LOGIT_TOL) -> bool:
+    """o = the oracle's tree verification; g_* from the GPU.  Returns whether
+    the GPU took the oracle's path."""
+    n = len(tokens) - 1
+    d = np.abs(o["logits"] - g_logits[: n + 1])
+    err = float(d.max())
+    assert np.isfinite(g_logits[: n + 1]).all(), f"{tag}: non-finite GPU logits"
+    assert err <= tol, f"{tag}: logits max-abs error {err:.4g} > {tol:.4g}"
+    gap = top2_gap(o["logits"])
+    g_greedy = argmax_lowest(g_logits[: n + 1])
+    o_greedy = argmax_lowest(o["logits"])
+    row_err = d.max(axis=1)
+    for i in range(n + 1):
+        if g_greedy[i] != o_greedy[i]:
+            assert gap[i] <= 2 * row_err[i] + 1e-6, \
+                f"{tag}: node {i} argmax differs although every logit is within half the gap"
+            report.append(f"{tag}: node {i} near-tie, oracle gap {gap[i]:.3g}")
+    # the GPU's acceptance must follow from its own greedy rows
+    want = tree_path_brute(tokens, parents, g_greedy)
+    assert list(g_path) == want, f"{tag}: GPU path {list(g_path)} != {want} from its own argmax"
+    assert (g_accept, g_next) == (len(want), int(g_greedy[([0] + want)[-1]])), f"{tag}: accept/next"
+    if (g_greedy == o_greedy).all():
+        assert list(g_path) == o["path"] and g_next == o["next"], f"{tag}: path differs from the oracle"
+        return True
+    report.append(f"{tag}: path {list(g_path)} vs oracle {o['path']} at a near-tie")
+    return list(g_path) == o["path"]

@@ -12,10 +12,10 @@ from oracle.accept import argmax_lowest
 from oracle.decoder import RequestKV, Weights
 from oracle.pages import PagePool
 from oracle.sampling import filtered_probs
-from oracle.verify import commit_request, greedy_decode, prefill_request, verify_request
+from oracle.verify import commit_request, greedy_decode, prefill_request, verify_request, verify_tree_request
 from paper_2607_17299_amd import synth
 from paper_2607_17299_amd.drafter import SuffixDrafter
-from parity import compare_request, shared_units
+from parity import compare_request, compare_tree_request, shared_units
 
 pytestmark = pytest.mark.gpu
 CFG = synth.TINY
@@ -385,6 +385,103 @@ def test_shared_prefix_cascade(tiny):
         np.testing.assert_allclose(g[0], K, atol=2e-2, rtol=2e-2)
         np.testing.assert_allclose(g[1], V, atol=2e-2, rtol=2e-2)
     print(f"\nshared-prefix cascade: reported {report}")
+
+
+def _tree_drafts(kind, rng, W, kv, pending, hist, drafter, k):
+    """(tokens, parents) of one request's draft tree, at most k nodes."""
+    if kind == 0:                                   # the host suffix drafter's tree
+        return drafter.propose_tree(hist + [pending], k)
+    if kind == 1:                                   # the greedy branch among distractors
+        g = greedy_decode(CFG, W, copy.deepcopy(kv), pending, 4)
+        x = [int(t) for t in rng.integers(0, CFG.vocab, 3)]
+        return [x[0], g[0], g[1], x[1], g[2], x[2], g[3]][:k], [0, 0, 2, 2, 3, 1, 5][:k]
+    if kind == 2:                                   # a random tree
+        n = int(rng.integers(1, k + 1))
+        return ([int(t) for t in rng.integers(0, CFG.vocab, n)],
+                [int(rng.integers(0, i + 1)) for i in range(n)])
+    return [], []                                   # no drafts: one decode row
+
+
+def test_tree_verification_matches_oracle(tiny):
+    """Draft trees (war_verify_step_tree), 4 requests x 512 cached tokens, at
+    most 8 nodes: a suffix-drafter tree, the greedy continuation placed among
+    distractor branches, a random tree, and no drafts, rotated over 3 steps.
+    Node logits, accepted path and next token against the oracle's tree
+    verification; after the commit the cache holds exactly the accepted path's
+    KV (the step moved it to consecutive slots).  Near-ties are reported; a
+    request whose path then differs ends the comparison of later steps."""
+    war, model, W = tiny["war"], tiny["model"], tiny["W"]
+    prior, ctxs = _tiny_workload(seed=11)
+    B, k = len(ctxs), 8
+    pool, seq, ctx, kvs, onext, *_ = _prefill_both(tiny, ctxs)
+    drafter = SuffixDrafter()
+    for p in prior:
+        drafter.add_trajectory(p)
+    hist = [list(c) for c in ctxs]
+    pending = [int(x) for x in onext]
+    rng = np.random.default_rng(11)
+    t = lambda a: torch.tensor(np.asarray(a), dtype=torch.int32, device=DEV)
+    report, greedy_hits = [], 0
+    for step in range(3):
+        trees = [_tree_drafts((step + b) % 4, rng, W, kvs[b], pending[b], hist[b], drafter, k)
+                 for b in range(B)]
+        dt, dp = np.zeros((B, k), np.int32), np.zeros((B, k), np.int32)
+        for b, (tk, par) in enumerate(trees):
+            dt[b, : len(tk)], dp[b, : len(par)] = tk, par
+        acc, nxt, path = t([0] * B), t([0] * B), t(np.zeros((B, k)))
+        logits = torch.full((B * (k + 1), CFG.vocab), float("nan"), device=DEV)
+        ctx_before = ctx.cpu().numpy().copy()
+        war.verify_step_tree(model, pool, seq, ctx, t(pending), t(dt), t(dp), t([len(x[0]) for x in trees]),
+                             k, acc, nxt, path, logits)
+        war.kv_commit(pool, seq, ctx, acc)
+        torch.cuda.synchronize()
+        g_acc, g_nxt, g_path = acc.cpu().numpy(), nxt.cpu().numpy(), path.cpu().numpy()
+        glog = logits.cpu().numpy().reshape(B, k + 1, CFG.vocab)
+        same = True
+        for b, (tk, par) in enumerate(trees):
+            tag = f"step {step} req {b}"
+            r = verify_tree_request(CFG, W, kvs[b], pending[b], tk, par)
+            a = int(g_acc[b])
+            assert (g_path[b, a:] == -1).all(), tag
+            ok = compare_tree_request(r, glog[b], [pending[b]] + tk, par, a, int(g_nxt[b]), g_path[b, :a],
+                                      report, tag)
+            if (step + b) % 4 == 1 and ok:
+                assert r["accept"] == 4 and a == 4, tag
+                greedy_hits += 1
+            if not ok:
+                same = False
+                continue
+            commit_request(kvs[b], r)
+            assert int(ctx.cpu()[b]) == kvs[b].length == int(ctx_before[b]) + a + 1, tag
+            for l in range(CFG.n_layers):
+                g = pool.gather_kv(b, kvs[b].length, l).double().cpu().numpy()
+                K, V = kvs[b].get(l)
+                np.testing.assert_allclose(g[0], K, atol=2e-2, rtol=2e-2, err_msg=tag)
+                np.testing.assert_allclose(g[1], V, atol=2e-2, rtol=2e-2, err_msg=tag)
+            hist[b] += [pending[b]] + [tk[i - 1] for i in r["path"]]
+            pending[b] = r["next"]
+        if not same:
+            break
+    assert pool.state()["status"] == 0
+    assert greedy_hits >= 2
+    print(f"\ntree verification: reported {report}")
+
+
+def test_tree_parent_out_of_range_is_flagged(tiny):
+    """A parent outside [0, i) sets the device error flag and is read as i - 1
+    (the step then verifies a chain)."""
+    war, model, W = tiny["war"], tiny["model"], tiny["W"]
+    _, ctxs = _tiny_workload(seed=12, B=1, ctx_len=40)
+    pool, seq, ctx, kvs, onext, *_ = _prefill_both(tiny, ctxs, pool_pages=16)
+    t = lambda a: torch.tensor(np.asarray(a), dtype=torch.int32, device=DEV)
+    g = greedy_decode(CFG, W, copy.deepcopy(kvs[0]), int(onext[0]), 3)
+    acc, nxt, path = t([0]), t([0]), t([[0, 0, 0]])
+    war.verify_step_tree(model, pool, seq, ctx, t([int(onext[0])]), t([g]), t([[0, 7, 2]]), None, 3,
+                         acc, nxt, path)
+    torch.cuda.synchronize()
+    assert pool.state()["status"] == -5          # WAR_ERR_DEVICE
+    a = int(acc.cpu()[0])
+    assert path.cpu().tolist()[0] == [1, 2, 3][:a] + [-1] * (3 - a)
 
 
 def _near_decision(logits, T, top_k, err, margins):
