@@ -59,7 +59,7 @@ def timed_steps(ds, model, pool, steps: int):
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(steps):
-        ds.verify(model, pool)
+        ds.run(model, pool)
         ds.commit(pool, discard=True)
     torch.cuda.synchronize()
     return (time.perf_counter() - t0) * 1e3 / steps
@@ -295,6 +295,20 @@ def main():
         variants["sibling_drafts"] = {"ms_per_step": round(ms2, 4),
                                       "accepted_tokens_per_s": round(float((acc2 + 1).sum() / (ms2 / 1e3)), 1),
                                       "accept_lens": acc2.tolist()}
+        if args.workload == "low_load":
+            # three siblings per request that leave the target's continuation at
+            # different tokens: a k-token chain against a k-node tree
+            sets = harness.diverging_siblings(cont, 3, cfg.vocab)
+            for name, tree in (("diverging_siblings_chain", False), ("diverging_siblings_tree", True)):
+                ds3 = harness.DeviceStep(harness.low_load_step(sibling_sets=sets, tree=tree))
+                for _ in range(2):
+                    ds3.run(model, pool)
+                    ds3.commit(pool, discard=True)
+                ms3 = timed_steps(ds3, model, pool, args.steps)
+                acc3 = ds3.accept.cpu().numpy()
+                variants[name] = {"ms_per_step": round(ms3, 4),
+                                  "accepted_tokens_per_s": round(float((acc3 + 1).sum() / (ms3 / 1e3)), 1),
+                                  "accept_lens": acc3.tolist()}
 
     if not args.no_variants:
         # sampled verification in the paper's setting (temperature 1, top-k 200),

@@ -24,9 +24,10 @@ war_status war_debug_mfma16(const void* A, const void* B, float* C, void* stream
  * output; "q" bf16 rotated queries [rows][nq*hd]; "o" bf16 attention output
  * [rows][nq*hd]; "P" fp32 split-K partials; "pm", "pl", "po" attention
  * partials; "rows", "reqs", "items" step metadata; "order" the attention work
- * order and "n_items" its counts (item slots, ordinary units, shared-prefix
- * units).  The pointer stays valid
- * until the next call on the model. */
+ * order and "n_items" its counts ([0] item slots, [1] units in the work
+ * order); "tree" the last tree step's node slots and node masks
+ * (int32 [2][max_rows]).  The pointer stays valid until the next call on the
+ * model. */
 war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes);
 
 /* The sampled-verification decision kernels alone (those war_verify_step_sampled

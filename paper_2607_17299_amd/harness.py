@@ -52,6 +52,7 @@ class Step:
     last_tokens: np.ndarray
     drafts: List[List[int]]
     k_max: int
+    parents: Optional[List[List[int]]] = None   # tree drafts: parent of node i+1 in [0, i]
 
     @property
     def B(self) -> int:
@@ -61,6 +62,12 @@ class Step:
         a = np.zeros((self.B, max(self.k_max, 1)), np.int32)
         for b, d in enumerate(self.drafts):
             a[b, : len(d)] = d
+        return a
+
+    def parent_array(self) -> np.ndarray:
+        a = np.zeros((self.B, max(self.k_max, 1)), np.int32)
+        for b, p in enumerate(self.parents):
+            a[b, : len(p)] = p
         return a
 
     def draft_lens(self) -> np.ndarray:
@@ -86,10 +93,25 @@ class DeviceStep:
         self.discard = torch.full((st.B,), -1, dtype=torch.int32, device=device)
         self.logits = (torch.empty((st.B * (st.k_max + 1), vocab), dtype=torch.float32, device=device)
                        if with_logits else None)
+        self.parents = t(st.parent_array()) if st.parents is not None else None
+        self.path = (torch.full((st.B, max(st.k_max, 1)), -1, dtype=torch.int32, device=device)
+                     if st.parents is not None else None)
 
     def verify(self, model: war.Model, pool: war.Pool, logits: bool = False):
         war.verify_step(model, pool, self.seq, self.ctx, self.last, self.drafts, self.dlens,
                         self.step.k_max, self.accept, self.next, self.logits if logits else None)
+
+    def verify_tree(self, model: war.Model, pool: war.Pool, logits: bool = False):
+        war.verify_step_tree(model, pool, self.seq, self.ctx, self.last, self.drafts, self.parents, self.dlens,
+                             self.step.k_max, self.accept, self.next, self.path,
+                             self.logits if logits else None)
+
+    def run(self, model: war.Model, pool: war.Pool, logits: bool = False):
+        """The step's verify call: tree drafts when the step has parents."""
+        if self.parents is not None:
+            self.verify_tree(model, pool, logits)
+        else:
+            self.verify(model, pool, logits)
 
     def verify_sampled(self, model: war.Model, pool: war.Pool, uniforms: torch.Tensor,
                        temperature: float = 1.0, top_k: int = 200):
@@ -130,18 +152,42 @@ def low_load_tokens(seed: int = 2, B: int = 8, ctx: int = 32768, n_prior: int = 
 
 
 def low_load_step(seed: int = 2, B: int = 8, ctx: int = 32768, k: int = 8, n_prior: int = 64,
-                  vocab: int = 151936, siblings: Optional[List[List[int]]] = None) -> Step:
+                  vocab: int = 151936, siblings: Optional[List[List[int]]] = None,
+                  sibling_sets: Optional[List[List[List[int]]]] = None, tree: bool = False) -> Step:
+    """siblings: per request, one sibling rollout's continuation of the same
+    context (GRPO siblings); sibling_sets: several per request.  tree: draft
+    trees of up to k nodes instead of k-token chains."""
     contexts, prior = low_load_tokens(seed, B, ctx, n_prior, ctx, vocab)
     d = SuffixDrafter()
     for p in prior:
         d.add_trajectory(p)
-    if siblings is not None:
-        # a sibling rollout that already produced this continuation (GRPO siblings)
+    sets = sibling_sets or ([[s] for s in siblings] if siblings is not None else None)
+    if sets is not None:
         for b in range(B):
-            d.add_trajectory(np.concatenate([contexts[b][-64:], siblings[b]]))
+            for sib in sets[b]:
+                d.add_trajectory(np.concatenate([contexts[b][-64:], sib]))
+    last = np.array([c[-1] for c in contexts], np.int32)
+    if tree:
+        trees = [d.propose_tree(contexts[b], k) for b in range(B)]
+        return Step(np.arange(B, dtype=np.int32), np.full(B, ctx, np.int32), last,
+                    [t[0] for t in trees], k, [t[1] for t in trees])
     drafts = [d.propose(contexts[b], k) for b in range(B)]
-    return Step(np.arange(B, dtype=np.int32), np.full(B, ctx, np.int32),
-                np.array([c[-1] for c in contexts], np.int32), drafts, k)
+    return Step(np.arange(B, dtype=np.int32), np.full(B, ctx, np.int32), last, drafts, k)
+
+
+def diverging_siblings(cont: List[List[int]], seed: int, vocab: int) -> List[List[List[int]]]:
+    """Three sibling continuations per request, added in this order: one that
+    leaves the target's continuation at its first token, one that leaves it at
+    its third, and the target's own."""
+    rng = np.random.default_rng([seed, 43])
+    out = []
+    for c in cont:
+        a, b = list(c), list(c)
+        a[0] = (a[0] + 1 + int(rng.integers(vocab - 1))) % vocab
+        if len(b) > 2:
+            b[2] = (b[2] + 1 + int(rng.integers(vocab - 1))) % vocab
+        out.append([a, b, list(c)])
+    return out
 
 
 def high_load_step(seed: int = 0, B: int = 64, k: int = 0, vocab: int = 151936,

@@ -18,9 +18,9 @@ import pytest
 import torch
 
 from oracle.decoder import RequestKV, Weights, forward_block
-from oracle.verify import greedy_decode, prefill_request, verify_request
+from oracle.verify import greedy_decode, prefill_request, verify_request, verify_tree_request
 from paper_2607_17299_amd import harness, synth
-from parity import compare_request, fp32_drift_tol, shared_units
+from parity import compare_request, compare_tree_request, fp32_drift_tol, shared_units
 
 pytestmark = pytest.mark.gpu
 KV_SEED = 9
@@ -91,6 +91,78 @@ def test_reduced_depth_verify_matches_oracle(large2, k, lens, ctxs):
     report = []
     err = _check_step(large2, st, report, f"k={k}")
     print(f"\nk={k}: max logit err {err:.3e}; reported {report}")
+
+
+@pytest.mark.parametrize("k", [3, 11])
+def test_reduced_depth_tree_matches_oracle(large2, k):
+    """Tree drafts on the 36-layer shapes (2 layers): random trees of ragged
+    sizes (k = 11 fills the 48-row attention block), contexts across several
+    key chunks and off page boundaries.  Node logits, accepted path, next
+    token; after the commit the last layer's cache of the new slots is the
+    accepted path's KV."""
+    cfg, model, W = large2["cfg"], large2["model"], large2["W"]
+    ctxs = [1500, 3001, 2048, 77]
+    B = len(ctxs)
+    rng = np.random.default_rng(100 + k)
+    sizes = [k, int(rng.integers(1, k + 1)), 0, k]
+    drafts = [rng.integers(0, cfg.vocab, n).tolist() for n in sizes]
+    parents = [[int(rng.integers(0, i + 1)) for i in range(n)] for n in sizes]
+    st = harness.Step(np.arange(B, dtype=np.int32), np.array(ctxs, np.int32),
+                      synth.uniform_tokens(k + 90, B, cfg.vocab), drafts, k, parents)
+    pool = harness.make_pool(cfg, st.ctx_lens, k + 2)
+    harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, KV_SEED)
+    ds = harness.DeviceStep(st, with_logits=True, vocab=cfg.vocab)
+    ds.verify_tree(model, pool, logits=True)
+    ds.commit(pool, discard=False)
+    torch.cuda.synchronize()
+    glog = ds.logits.cpu().numpy().reshape(B, k + 1, cfg.vocab)
+    acc, nxt, path = ds.accept.cpu().numpy(), ds.next.cpu().numpy(), ds.path.cpu().numpy()
+    report = []
+    for b in range(B):
+        tag = f"k={k} req {b}"
+        kv = RequestKV(cfg, [_oracle_kv(cfg, b, ctxs[b])(l) for l in range(cfg.n_layers)])
+        r = verify_tree_request(cfg, W, kv, int(st.last_tokens[b]), drafts[b], parents[b])
+        a = int(acc[b])
+        same = compare_tree_request(r, glog[b], [int(st.last_tokens[b])] + drafts[b], parents[b], a,
+                                    int(nxt[b]), path[b, :a], report, tag)
+        if same:
+            g = pool.gather_kv(b, ctxs[b] + a + 1, cfg.n_layers - 1).double().cpu().numpy()
+            nk, nv = r["new_kv"][cfg.n_layers - 1]
+            np.testing.assert_allclose(g[0][:, ctxs[b]:], nk, atol=3e-2, rtol=2e-2, err_msg=tag)
+            np.testing.assert_allclose(g[1][:, ctxs[b]:], nv, atol=3e-2, rtol=2e-2, err_msg=tag)
+    np.testing.assert_array_equal(ds.ctx.cpu().numpy(), st.ctx_lens + acc + 1)
+    print(f"\ntree k={k}: reported {report}")
+
+
+def test_reduced_depth_tree_greedy_branch_accepted(large2):
+    """A tree holding the target's greedy continuation on one branch, under
+    distractor branches (decisive LM head): the GPU accepts exactly that
+    branch, and the emitted tokens are the greedy stream."""
+    war, cfg = large2["war"], large2["cfg"]
+    w = harness.large_weights(cfg, lm_std=0.2)
+    model = war.Model(cfg, w, max_rows=64)
+    W = Weights(cfg, w)
+    ctxs = np.array([1200, 2000], np.int32)
+    last = synth.uniform_tokens(62, 2, cfg.vocab)
+    rng = np.random.default_rng(62)
+    drafts, parents, conts = [], [], []
+    for b in range(2):
+        kv = RequestKV(cfg, [_oracle_kv(cfg, b, int(ctxs[b]))(l) for l in range(cfg.n_layers)])
+        g = greedy_decode(cfg, W, kv, int(last[b]), 5)
+        x = [int(v) for v in rng.integers(0, cfg.vocab, 4)]
+        # greedy branch 2 -> 3 -> 6 -> 8; distractors 1, 4, 5, 7
+        drafts.append([x[0], g[0], g[1], x[1], x[2], g[2], x[3], g[3]])
+        parents.append([0, 0, 2, 2, 1, 3, 6, 6])
+        conts.append(g)
+    st = harness.Step(np.arange(2, dtype=np.int32), ctxs, last, drafts, 8, parents)
+    pool = harness.make_pool(cfg, st.ctx_lens, 10)
+    harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, KV_SEED)
+    ds = harness.DeviceStep(st)
+    ds.verify_tree(model, pool)
+    ds.commit(pool, discard=False)
+    assert ds.accept.cpu().tolist() == [4, 4]
+    assert ds.path.cpu().numpy()[:, :4].tolist() == [[2, 3, 6, 8]] * 2
+    assert ds.next.cpu().tolist() == [c[4] for c in conts]
 
 
 def test_reduced_depth_sibling_drafts_accepted(large2):
