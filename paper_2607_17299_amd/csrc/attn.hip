@@ -9,17 +9,23 @@
 // Work item = (request, row block, key chunk) x kv-head, listed on the device
 // by the step setup; a persistent grid strides over the items.  Inside an item
 // the 4 waves split the chunk's keys; each wave walks 32-key blocks (two pages):
-//   S^T = K Q^T  -- v_mfma_f32_16x16x32_bf16 with the keys as the M side: lane
-//                   (m, g) loads 64 contiguous bytes of one key row, and key
-//                   m of tile t is chosen as (m/4)*8 + 4t + m%4 so that every
-//                   lane ends up holding 8 consecutive keys of one query row;
-//   online softmax in fp32 (exp2, running max/sum per query row), P rounded
-//                   to bf16 for the second product;
+//   S^T = K Q^T  -- v_mfma_f32_16x16x32_bf16 with the keys as the M side:
+//                   k-step j covers dims 32j..32j+31, so the 4 lane groups of
+//                   one load read 64 contiguous bytes of each of 16 key rows;
+//                   key m of tile t is chosen as (m/4)*8 + 4t + m%4 so that
+//                   every lane ends up holding 8 consecutive keys of one row;
+//   online softmax in fp32 (exp2, running max/sum per query row), P split
+//                   into bf16 hi + lo for the second product;
 //   O^T += V^T P^T -- V is stored transposed inside a page ([dim][slot]), so
 //                   each lane reads 16 contiguous bytes (8 keys of one dim).
+// Block bookkeeping (positions, page ids, page bases) is wave-uniform and kept
+// in scalar registers; only the last blocks of a request take the causal /
+// tree / end-of-sequence masks, in a loop of their own.
 // The waves' (max, sum, O) are merged through LDS in a fixed order and one
 // partial per item goes to global memory; the combine kernel merges a
 // request's chunks in item order (deterministic).
+#include <type_traits>
+
 #include "kernels.h"
 
 namespace {
@@ -39,7 +45,7 @@ struct KVFrag {
   uint4 v[HD / 16];
 };
 
-// DEPTH = blocks in flight per wave beyond the one being computed (0, 1 or 2);
+// DEPTH = blocks in flight per wave beyond the one being computed (0 or 1);
 // QLDS = queries read from LDS instead of registers; WPE = waves per SIMD the
 // register budget allows.  Two waves per SIMD let one wave's MFMA/softmax work
 // overlap the other's memory waits.
@@ -47,7 +53,6 @@ struct KVFrag {
 template <int NR, int HD, int DEPTH, bool QLDS, int WPE, bool TREE>
 __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(WPE, WPE)))
 k_attn(AttnArgs a) {
-  constexpr int DPL = HD / 4;    // dims per lane group in the S^T operands
   constexpr int KSUB = HD / 32;  // MFMA k-steps over the head dim
   constexpr int NDT = HD / 16;   // 16-dim output tiles
   constexpr int RB = NR * 16;
@@ -57,11 +62,20 @@ k_attn(AttnArgs a) {
   __shared__ float s_o[RB * OST];
   __shared__ __attribute__((aligned(16))) bf16_t s_q[QLDS ? RB * QST : 8];
   __shared__ uint32_t s_tm[TREE ? RB : 1];  // tree drafts: step slots each row sees
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
+  const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
+  // the wave index is wave-uniform: block positions, page ids and page bases
+  // derived from it live in scalar registers
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int total = (a.meta.order ? a.meta.n_items[1] : a.meta.n_items[0]) * a.n_kv_heads;
   const int P = a.kv.page_size;
   // key row of this lane in S^T tile t (within a 32-key block); tile 1 adds 4
   const int kk0 = (ln >> 2) * 8 + (ln & 3);
+  // Per-lane element offsets inside a page (kind 0 = K [slot][dim], kind 1 =
+  // V^T [dim][slot]): lanes ln < 8 read K rows of the block's first page, the
+  // others its second; lane groups lg < 2 read V^T of the first page.
+  const int koff0 = (kk0 & 15) * HD + lg * 8, koff1 = ((kk0 + 4) & 15) * HD + lg * 8;
+  const int voff = P * HD + (lg & 1) * 8 + ln * P;
+  const bool k_second = ln >= 8, v_second = lg >= 2;
 
   for (int it = blockIdx.x; it < total; it += gridDim.x) {
     // units in work order; with 8 kv-heads (a multiple of 8 in general) every
@@ -148,9 +162,9 @@ k_attn(AttnArgs a) {
         int qrow, h;
         int64_t prow;
         if (row_src(r, qrow, h, prow)) {
-          const bf16_t* qp = a.q + (int64_t)qrow * a.q_stride + h * HD + lg * DPL;
+          const bf16_t* qp = a.q + (int64_t)qrow * a.q_stride + h * HD + lg * 8;
 #pragma unroll
-          for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + j * 8));
+          for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + j * 32));
         } else {
 #pragma unroll
           for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(make_uint4(0, 0, 0, 0));
@@ -159,7 +173,7 @@ k_attn(AttnArgs a) {
     }
     auto qfrag = [&](int rt, int j) -> bf16x8 {
       if constexpr (QLDS)
-        return as_bf16x8(*reinterpret_cast<const uint4*>(&s_q[(rt * 16 + ln) * QST + lg * DPL + j * 8]));
+        return as_bf16x8(*reinterpret_cast<const uint4*>(&s_q[(rt * 16 + ln) * QST + j * 32 + lg * 8]));
       else
         return qf[rt][j];
     };
@@ -177,34 +191,32 @@ k_attn(AttnArgs a) {
     const int CW = a.chunk / 4;
     const int wk0 = kbeg + w * CW, wk1 = min(kend, wk0 + CW);
     const int nb = wk1 > wk0 ? (wk1 - wk0 + 31) / 32 : 0;
+    // blocks before nfull lie at or below every row's position (and inside the
+    // sequence): no causal, tree or end-of-sequence mask
+    const int nfull = mask_from - 31 - wk0 < 0 ? 0 : min(nb, (mask_from - 31 - wk0) / 32 + 1);
     const int32_t* trow = a.table + (int64_t)seq * a.max_pages;
-    const bf16_t* kvl = a.kv.kv;
+    // elements per page across kv-heads and kinds; this kv-head's part of page 0
+    const int64_t pstride = (int64_t)a.kv.n_kv_heads * 2 * P * HD;
+    const bf16_t* kvb = a.kv.kv + a.kv.page_elems(a.layer, 0, kvh, 0);
 
     auto load_block = [&](KVFrag<HD>& f, int kb) {
       const int pg0 = trow[kb / P];
       const int pg1 = (kb + 16 < S) ? trow[kb / P + 1] : pg0;
+      const bf16_t* kp = kvb + (int64_t)(k_second ? pg1 : pg0) * pstride;
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const int kk = kk0 + 4 * t;
-        const int pg = kk < 16 ? pg0 : pg1;
-        const bf16_t* kp = kvl + a.kv.page_elems(a.layer, pg, kvh, 0) + (kk & 15) * HD + lg * DPL;
-#pragma unroll
-        for (int j = 0; j < KSUB; ++j) f.k[t][j] = *reinterpret_cast<const uint4*>(kp + j * 8);
+      for (int j = 0; j < KSUB; ++j) {
+        f.k[0][j] = *reinterpret_cast<const uint4*>(kp + koff0 + j * 32);
+        f.k[1][j] = *reinterpret_cast<const uint4*>(kp + koff1 + j * 32);
       }
-      const int pg = lg < 2 ? pg0 : pg1;
-      const bf16_t* vp = kvl + a.kv.page_elems(a.layer, pg, kvh, 1) + (lg & 1) * 8;
+      const bf16_t* vp = kvb + (int64_t)(v_second ? pg1 : pg0) * pstride + voff;
 #pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) f.v[dt] = *reinterpret_cast<const uint4*>(vp + (dt * 16 + ln) * P);
-      if (kb + 32 > S) {  // the sequence ends inside this block
-        const int nvalid = min(max(S - (kb + lg * 8), 0), 8);
-#pragma unroll
-        for (int dt = 0; dt < NDT; ++dt) f.v[dt] = keep_first(f.v[dt], nvalid);
-      }
+      for (int dt = 0; dt < NDT; ++dt) f.v[dt] = *reinterpret_cast<const uint4*>(vp + dt * 16 * P);
     };
 
-    auto compute_block = [&](const KVFrag<HD>& f, int kb) {
-      // keys of this block above the smallest row position need the causal mask
-      const bool tail = kb + 31 > mask_from;
+    // MASK: the block holds keys above some row's position or past the
+    // sequence end (only the last blocks of a request)
+    auto compute_block = [&](const KVFrag<HD>& fin, int kb, auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
       if constexpr (QLDS) asm volatile("" ::: "memory");  // re-read Q from LDS each block
       // phase 1: scores of every row tile (the K fragments die after this)
       float sc[NR][8];
@@ -214,8 +226,8 @@ k_attn(AttnArgs a) {
 #pragma unroll
         for (int j = 0; j < KSUB; ++j) {
           const bf16x8 q = qfrag(rt, j);
-          s0 = mfma16(as_bf16x8(f.k[0][j]), q, s0);
-          s1 = mfma16(as_bf16x8(f.k[1][j]), q, s1);
+          s0 = mfma16(as_bf16x8(fin.k[0][j]), q, s0);
+          s1 = mfma16(as_bf16x8(fin.k[1][j]), q, s1);
         }
         // lane holds S^T[key kb + lg*8 + 4t + i][row rt*16 + ln]
 #pragma unroll
@@ -224,11 +236,21 @@ k_attn(AttnArgs a) {
           sc[rt][4 + i] = s1[i];
         }
       }
+      uint4 vf[NDT];
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) vf[dt] = fin.v[dt];
+      if constexpr (MASK) {
+        if (kb + 32 > S) {  // the sequence ends inside this block
+          const int nvalid = min(max(S - (kb + lg * 8), 0), 8);
+#pragma unroll
+          for (int dt = 0; dt < NDT; ++dt) vf[dt] = keep_first(vf[dt], nvalid);
+        }
+      }
       // phase 2: online softmax and O^T += V^T P^T per row tile
 #pragma unroll
       for (int rt = 0; rt < NR; ++rt) {
         float* sv = sc[rt];
-        if (tail) {
+        if constexpr (MASK) {
           if constexpr (TREE) {
             // a tree row sees the step slot pos0 + i only when node i is on its path
             const uint32_t tm = s_tm[rt * 16 + ln];
@@ -263,13 +285,14 @@ k_attn(AttnArgs a) {
           }
         }
         const float m_use = m_run[rt] == -INFINITY ? 0.f : m_run[rt];
-        // P = hi + lo, both bf16: the product keeps ~16 bits of each weight
+        // P = hi + lo, both bf16: the product keeps ~16 bits of each weight.
+        // v_exp_f32 directly: weights below 2^-126 of the running max flush to 0.
         float sum = 0.f;
         uint32_t hi[4], lo[4];
 #pragma unroll
         for (int e = 0; e < 8; e += 2) {
-          const float p0 = exp2f(fmaf(sv[e], a.scale_log2, -m_use));
-          const float p1 = exp2f(fmaf(sv[e + 1], a.scale_log2, -m_use));
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[e], a.scale_log2, -m_use));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[e + 1], a.scale_log2, -m_use));
           sum += p0 + p1;
           hi[e / 2] = pack2(p0, p1);
           lo[e / 2] = pack2(p0 - lo_f(hi[e / 2]), p1 - hi_f(hi[e / 2]));
@@ -279,47 +302,44 @@ k_attn(AttnArgs a) {
         const bf16x8 pl = as_bf16x8(make_uint4(lo[0], lo[1], lo[2], lo[3]));
 #pragma unroll
         for (int dt = 0; dt < NDT; ++dt) {
-          o_acc[dt][rt] = mfma16(as_bf16x8(f.v[dt]), ph, o_acc[dt][rt]);
-          o_acc[dt][rt] = mfma16(as_bf16x8(f.v[dt]), pl, o_acc[dt][rt]);
+          o_acc[dt][rt] = mfma16(as_bf16x8(vf[dt]), ph, o_acc[dt][rt]);
+          o_acc[dt][rt] = mfma16(as_bf16x8(vf[dt]), pl, o_acc[dt][rt]);
         }
       }
     };
+    using NoMask = std::integral_constant<bool, false>;
+    using Mask = std::integral_constant<bool, true>;
 
-    // Block i of this wave is at key wk0 + 32 i; blocks in flight rotate through
-    // DEPTH + 1 register sets (static indexing: the loop is unrolled by DEPTH + 1).
-    if constexpr (DEPTH == 0) {
-      KVFrag<HD> f0;
-      for (int i = 0; i < nb; ++i) {
-        load_block(f0, wk0 + 32 * i);
-        compute_block(f0, wk0 + 32 * i);
+    // Block i of this wave is at key wk0 + 32 i.  The unmasked blocks and the
+    // masked tail (at most the last two blocks of a request) run in separate
+    // loops, so that each loop body holds one instantiation of the block code.
+    int i = 0;
+    KVFrag<HD> f0;
+    if constexpr (DEPTH == 1) {
+      // one block in flight beyond the one being computed: f0 holds block i at
+      // the top of each iteration
+      KVFrag<HD> f1;
+      if (nfull > 0) load_block(f0, wk0);
+      for (; i + 1 < nfull; i += 2) {
+        load_block(f1, wk0 + 32 * (i + 1));
+        compute_block(f0, wk0 + 32 * i, NoMask{});
+        if (i + 2 < nfull) load_block(f0, wk0 + 32 * (i + 2));
+        compute_block(f1, wk0 + 32 * (i + 1), NoMask{});
       }
-    } else if constexpr (DEPTH == 1) {
-      KVFrag<HD> f0, f1;
-      if (nb > 0) load_block(f0, wk0);
-      for (int i = 0; i < nb; i += 2) {
-        if (i + 1 < nb) load_block(f1, wk0 + 32 * (i + 1));
-        compute_block(f0, wk0 + 32 * i);
-        if (i + 1 < nb) {
-          if (i + 2 < nb) load_block(f0, wk0 + 32 * (i + 2));
-          compute_block(f1, wk0 + 32 * (i + 1));
-        }
+      if (i < nfull) {
+        compute_block(f0, wk0 + 32 * i, NoMask{});
+        ++i;
       }
     } else {
-      KVFrag<HD> f0, f1, f2;
-      if (nb > 0) load_block(f0, wk0);
-      if (nb > 1) load_block(f1, wk0 + 32);
-      for (int i = 0; i < nb; i += 3) {
-        if (i + 2 < nb) load_block(f2, wk0 + 32 * (i + 2));
-        compute_block(f0, wk0 + 32 * i);
-        if (i + 1 < nb) {
-          if (i + 3 < nb) load_block(f0, wk0 + 32 * (i + 3));
-          compute_block(f1, wk0 + 32 * (i + 1));
-        }
-        if (i + 2 < nb) {
-          if (i + 4 < nb) load_block(f1, wk0 + 32 * (i + 4));
-          compute_block(f2, wk0 + 32 * (i + 2));
-        }
+      static_assert(DEPTH == 0, "blocks in flight: 0 or 1");
+      for (; i < nfull; ++i) {
+        load_block(f0, wk0 + 32 * i);
+        compute_block(f0, wk0 + 32 * i, NoMask{});
       }
+    }
+    for (; i < nb; ++i) {
+      load_block(f0, wk0 + 32 * i);
+      compute_block(f0, wk0 + 32 * i, Mask{});
     }
 
     // ---- merge the 4 waves (fixed order) and write the item's partial
@@ -385,63 +405,63 @@ k_attn(AttnArgs a) {
 }
 
 // Merge a (request, row block)'s chunk partials in item order; o = sum / l -> bf16.
-// Workgroup = (segment, kv-head, 16-row slice): the per-item weights
-// exp2(m_i - m) / l of its rows go to LDS, then every thread accumulates float4
-// runs of the output with all of its loads independent.
+// Workgroup = (segment, kv-head, slice of 1024/HD rows: 8 at head_dim 128), so
+// a step's merge spreads over hundreds of workgroups.  One wave per row puts
+// the per-item weights exp2(m_i - m) in LDS (lanes over items), then one thread
+// per output float4 accumulates the items in order with independent loads.
 constexpr int kCombMaxItems = 512;
 template <int RB, int HD>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
-  __shared__ float s_w[16][kCombMaxItems];
-  __shared__ float s_mx[16];
-  const int seg = blockIdx.x, kvh = blockIdx.y, r0 = blockIdx.z * 16;
+  constexpr int TPR = HD / 4;     // threads per row
+  constexpr int RPW = 256 / TPR;  // rows per workgroup
+  __shared__ float s_w[RPW][kCombMaxItems];
+  __shared__ float s_il[RPW];
+  const int seg = blockIdx.x, kvh = blockIdx.y, r0 = blockIdx.z * RPW;
   const int b = a.meta.seg_req[seg];
   const int t0 = a.meta.seg_rb[seg] * a.TB;
-  const int nt = min(a.TB, a.meta.req_ntok[b] - t0);
-  const int nrows = nt * a.G;
-  if (nt <= 0 || r0 >= nrows) return;
-  const int rows = min(16, nrows - r0);
+  const int nrows = min(a.TB, a.meta.req_ntok[b] - t0) * a.G;
+  if (r0 >= nrows) return;
+  const int rows = min(RPW, nrows - r0);
   const int ib = a.meta.seg_begin[seg], ni = min(a.meta.seg_count[seg], kCombMaxItems);
-  const int row0 = a.meta.req_row0[b];
+  const int64_t is = (int64_t)a.n_kv_heads * RB;  // pm / pl elements per item
+  const float* pm = a.pm + ((int64_t)ib * a.n_kv_heads + kvh) * RB + r0;
+  const float* pl = a.pl + ((int64_t)ib * a.n_kv_heads + kvh) * RB + r0;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  // one wave per row: max, then the normalised weights
   for (int r = w; r < rows; r += 4) {
     float mm = -INFINITY;
-    for (int i = lane; i < ni; i += 64)
-      mm = fmaxf(mm, a.pm[((int64_t)(ib + i) * a.n_kv_heads + kvh) * RB + r0 + r]);
+    for (int i = lane; i < ni; i += 64) mm = fmaxf(mm, pm[i * is + r]);
     mm = wave_max(mm);
     float l = 0.f;
     for (int i = lane; i < ni; i += 64) {
-      const int64_t pb = ((int64_t)(ib + i) * a.n_kv_heads + kvh) * RB + r0 + r;
-      const float f = exp2f(a.pm[pb] - mm);
+      const float f = exp2f(pm[i * is + r] - mm);
       s_w[r][i] = f;
-      l += a.pl[pb] * f;
+      l += pl[i * is + r] * f;
     }
     l = wave_sum(l);
-    if (lane == 0) s_mx[r] = 1.f / l;
+    if (lane == 0) s_il[r] = 1.f / l;
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < rows * (HD / 4); e += blockDim.x) {
-    const int r = e / (HD / 4), d4 = (e % (HD / 4)) * 4;
-    float4 acc = {0.f, 0.f, 0.f, 0.f};
-    const float* base = a.po + ((int64_t)ib * a.n_kv_heads + kvh) * RB * HD + (int64_t)(r0 + r) * HD + d4;
-    const int64_t stride = (int64_t)a.n_kv_heads * RB * HD;
-    for (int i = 0; i < ni; ++i) {
-      const float4 v = *reinterpret_cast<const float4*>(base + i * stride);
-      const float f = s_w[r][i];
-      acc.x += v.x * f;
-      acc.y += v.y * f;
-      acc.z += v.z * f;
-      acc.w += v.w * f;
-    }
-    const float inv = s_mx[r];
-    const int rr = r0 + r;
-    const int ti = t0 + rr / a.G, h = kvh * a.G + rr % a.G;
-    bf16_t* dst = a.o + (int64_t)(row0 + ti) * a.q_stride + h * HD + d4;
-    uint2 o;
-    o.x = pack2(acc.x * inv, acc.y * inv);
-    o.y = pack2(acc.z * inv, acc.w * inv);
-    *reinterpret_cast<uint2*>(dst) = o;
+  const int r = threadIdx.x / TPR, d4 = (threadIdx.x % TPR) * 4;
+  if (r >= rows) return;
+  const float* po = a.po + (((int64_t)ib * a.n_kv_heads + kvh) * RB + r0 + r) * HD + d4;
+  float4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 8
+  for (int i = 0; i < ni; ++i) {
+    const float4 v = *reinterpret_cast<const float4*>(po + i * is * HD);
+    const float f = s_w[r][i];
+    acc.x += v.x * f;
+    acc.y += v.y * f;
+    acc.z += v.z * f;
+    acc.w += v.w * f;
   }
+  const float inv = s_il[r];
+  const int rr = r0 + r;
+  const int ti = t0 + rr / a.G, h = kvh * a.G + rr % a.G;
+  bf16_t* dst = a.o + (int64_t)(a.meta.req_row0[b] + ti) * a.q_stride + h * HD + d4;
+  uint2 o;
+  o.x = pack2(acc.x * inv, acc.y * inv);
+  o.y = pack2(acc.z * inv, acc.w * inv);
+  *reinterpret_cast<uint2*>(dst) = o;
 }
 
 // Tuned per row-tile count: one tile prefetches one block and keeps Q in
@@ -467,7 +487,8 @@ void launch_attn_nr(const AttnArgs& a, int head_dim, int grid, hipStream_t st) {
 
 template <int RB>
 void launch_comb(const AttnArgs& a, int head_dim, int n_segs, hipStream_t st) {
-  dim3 grid(n_segs, a.n_kv_heads, RB / 16);
+  // slices only over the rows a segment can have (TB tokens x G heads)
+  dim3 grid(n_segs, a.n_kv_heads, cdiv_i(std::min(RB, a.TB * a.G), 1024 / head_dim));
   if (head_dim == 128)
     k_attn_combine<RB, 128><<<grid, 256, 0, st>>>(a);
   else
