@@ -77,10 +77,23 @@ k_attn(AttnArgs a) {
   const int voff = P * HD + (lg & 1) * 8 + ln * P;
   const bool k_second = ln >= 8, v_second = lg >= 2;
 
-  for (int it = blockIdx.x; it < total; it += gridDim.x) {
-    // units in work order; with 8 kv-heads (a multiple of 8 in general) every
-    // unit of one kv-head runs on the same XCD, so items that are neighbours in
-    // the order (the same prefix chunk of sibling requests) share its L2
+  // Units are handed out by per-class counters (class = workgroup id mod NC):
+  // a workgroup takes the next unit of its class when it finishes one, so
+  // units of unequal length balance over the workgroups.  Workgroups are dealt
+  // to the 8 XCDs round-robin, so with 8 kv-heads every unit of one kv-head
+  // runs on the same XCD, and items that are neighbours in the work order (the
+  // same prefix chunk of sibling requests) share its L2.  The combine kernel
+  // that follows every launch resets the counters.
+  const int NC = min(8, (int)gridDim.x);
+  const int cls = blockIdx.x % NC;
+  __shared__ int s_next;
+  for (;;) {
+    if (tid == 0) s_next = atomicAdd(&a.unit_ctr[cls], 1);
+    __syncthreads();
+    // (the loop body passes a barrier before thread 0 rewrites s_next)
+    const int it = s_next * NC + cls;
+    if (it >= total) break;
+    // units in work order
     const int slot = it / a.n_kv_heads, kvh = it % a.n_kv_heads;
     const int item = a.meta.order ? a.meta.order[slot] : slot;
     const int4 itm = a.meta.items[item];
@@ -117,6 +130,39 @@ k_attn(AttnArgs a) {
     }
     const int S = last_pos + 1;
     const int kbeg = chunk * a.chunk, kend = min(S, kbeg + a.chunk);
+    const int CW = a.chunk / 4;
+    const int wk0 = kbeg + w * CW, wk1 = min(kend, wk0 + CW);
+    const int nb = wk1 > wk0 ? (wk1 - wk0 + 31) / 32 : 0;
+    // blocks before nfull lie at or below every row's position (and inside the
+    // sequence): no causal, tree or end-of-sequence mask
+    const int nfull = mask_from - 31 - wk0 < 0 ? 0 : min(nb, (mask_from - 31 - wk0) / 32 + 1);
+    const int32_t* trow = a.table + (int64_t)seq * a.max_pages;
+    // elements per page across kv-heads and kinds; this kv-head's part of page 0
+    const int64_t pstride = (int64_t)a.kv.n_kv_heads * 2 * P * HD;
+    const bf16_t* kvb = a.kv.kv + a.kv.page_elems(a.layer, 0, kvh, 0);
+
+    auto load_block = [&](KVFrag<HD>& f, int kb) {
+      const int pg0 = trow[kb / P];
+      const int pg1 = (kb + 16 < S) ? trow[kb / P + 1] : pg0;
+      const bf16_t* kp = kvb + (int64_t)(k_second ? pg1 : pg0) * pstride;
+#pragma unroll
+      for (int j = 0; j < KSUB; ++j) {
+        f.k[0][j] = *reinterpret_cast<const uint4*>(kp + koff0 + j * 32);
+        f.k[1][j] = *reinterpret_cast<const uint4*>(kp + koff1 + j * 32);
+      }
+      const bf16_t* vp = kvb + (int64_t)(v_second ? pg1 : pg0) * pstride + voff;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) f.v[dt] = *reinterpret_cast<const uint4*>(vp + dt * 16 * P);
+    };
+
+    // The first block is requested before the queries are staged, and each
+    // next block as soon as the current one is computed -- except with three
+    // row tiles, which lack the registers for a block held across those points
+    // and load each block right before computing it.
+    constexpr bool kEarlyLoad = NR < 3;
+    KVFrag<HD> f0;
+    if (kEarlyLoad && nb > 0) load_block(f0, wk0);
+
     // row r -> (query row, query head) and its partial row; false if r is not live
     auto row_src = [&](int r, int& qrow, int& h, int64_t& prow) -> bool {
       if (r >= nrows) return false;
@@ -187,31 +233,6 @@ k_attn(AttnArgs a) {
 #pragma unroll
       for (int dt = 0; dt < NDT; ++dt) o_acc[dt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
     }
-
-    const int CW = a.chunk / 4;
-    const int wk0 = kbeg + w * CW, wk1 = min(kend, wk0 + CW);
-    const int nb = wk1 > wk0 ? (wk1 - wk0 + 31) / 32 : 0;
-    // blocks before nfull lie at or below every row's position (and inside the
-    // sequence): no causal, tree or end-of-sequence mask
-    const int nfull = mask_from - 31 - wk0 < 0 ? 0 : min(nb, (mask_from - 31 - wk0) / 32 + 1);
-    const int32_t* trow = a.table + (int64_t)seq * a.max_pages;
-    // elements per page across kv-heads and kinds; this kv-head's part of page 0
-    const int64_t pstride = (int64_t)a.kv.n_kv_heads * 2 * P * HD;
-    const bf16_t* kvb = a.kv.kv + a.kv.page_elems(a.layer, 0, kvh, 0);
-
-    auto load_block = [&](KVFrag<HD>& f, int kb) {
-      const int pg0 = trow[kb / P];
-      const int pg1 = (kb + 16 < S) ? trow[kb / P + 1] : pg0;
-      const bf16_t* kp = kvb + (int64_t)(k_second ? pg1 : pg0) * pstride;
-#pragma unroll
-      for (int j = 0; j < KSUB; ++j) {
-        f.k[0][j] = *reinterpret_cast<const uint4*>(kp + koff0 + j * 32);
-        f.k[1][j] = *reinterpret_cast<const uint4*>(kp + koff1 + j * 32);
-      }
-      const bf16_t* vp = kvb + (int64_t)(v_second ? pg1 : pg0) * pstride + voff;
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) f.v[dt] = *reinterpret_cast<const uint4*>(vp + dt * 16 * P);
-    };
 
     // MASK: the block holds keys above some row's position or past the
     // sequence end (only the last blocks of a request)
@@ -314,32 +335,36 @@ k_attn(AttnArgs a) {
     // masked tail (at most the last two blocks of a request) run in separate
     // loops, so that each loop body holds one instantiation of the block code.
     int i = 0;
-    KVFrag<HD> f0;
-    if constexpr (DEPTH == 1) {
-      // one block in flight beyond the one being computed: f0 holds block i at
-      // the top of each iteration
-      KVFrag<HD> f1;
-      if (nfull > 0) load_block(f0, wk0);
-      for (; i + 1 < nfull; i += 2) {
-        load_block(f1, wk0 + 32 * (i + 1));
-        compute_block(f0, wk0 + 32 * i, NoMask{});
-        if (i + 2 < nfull) load_block(f0, wk0 + 32 * (i + 2));
-        compute_block(f1, wk0 + 32 * (i + 1), NoMask{});
+    if constexpr (kEarlyLoad) {
+      // at the top of every iteration f0 holds block i
+      if constexpr (DEPTH == 1) {
+        // one more block in flight while a block is computed
+        KVFrag<HD> f1;
+        for (; i + 1 < nfull; i += 2) {
+          load_block(f1, wk0 + 32 * (i + 1));
+          compute_block(f0, wk0 + 32 * i, NoMask{});
+          if (i + 2 < nb) load_block(f0, wk0 + 32 * (i + 2));
+          compute_block(f1, wk0 + 32 * (i + 1), NoMask{});
+        }
       }
-      if (i < nfull) {
+      for (; i < nfull; ++i) {
         compute_block(f0, wk0 + 32 * i, NoMask{});
-        ++i;
+        if (i + 1 < nb) load_block(f0, wk0 + 32 * (i + 1));
+      }
+      for (; i < nb; ++i) {
+        compute_block(f0, wk0 + 32 * i, Mask{});
+        if (i + 1 < nb) load_block(f0, wk0 + 32 * (i + 1));
       }
     } else {
-      static_assert(DEPTH == 0, "blocks in flight: 0 or 1");
+      static_assert(DEPTH == 0, "a block in flight needs the early first load");
       for (; i < nfull; ++i) {
         load_block(f0, wk0 + 32 * i);
         compute_block(f0, wk0 + 32 * i, NoMask{});
       }
-    }
-    for (; i < nb; ++i) {
-      load_block(f0, wk0 + 32 * i);
-      compute_block(f0, wk0 + 32 * i, Mask{});
+      for (; i < nb; ++i) {
+        load_block(f0, wk0 + 32 * i);
+        compute_block(f0, wk0 + 32 * i, Mask{});
+      }
     }
 
     // ---- merge the 4 waves (fixed order) and write the item's partial
@@ -417,6 +442,8 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   __shared__ float s_w[RPW][kCombMaxItems];
   __shared__ float s_il[RPW];
   const int seg = blockIdx.x, kvh = blockIdx.y, r0 = blockIdx.z * RPW;
+  // the attention launch before this one is complete: its work counters restart
+  if (seg == 0 && kvh == 0 && blockIdx.z == 0 && threadIdx.x < 8) a.unit_ctr[threadIdx.x] = 0;
   const int b = a.meta.seg_req[seg];
   const int t0 = a.meta.seg_rb[seg] * a.TB;
   const int nrows = min(a.TB, a.meta.req_ntok[b] - t0) * a.G;

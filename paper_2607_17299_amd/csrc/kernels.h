@@ -67,6 +67,8 @@ struct AttnArgs {
   float* pl;         // [item][kvh][RB]
   float* po;         // [item][kvh][RB][head_dim]
   bf16_t* o;         // combine output [rows][n_q_heads * head_dim]
+  int32_t* unit_ctr; // [8] attention work counters; zero before each attention
+                     // launch (the combine kernel resets them)
 };
 
 // allocator / setup (alloc.hip)

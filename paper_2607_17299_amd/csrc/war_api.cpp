@@ -106,6 +106,7 @@ struct war_model {
   DevBuf reqs_i32;  // seq, pos0, ntok, row0      [4][n_req_cap]
   DevBuf segs_i32;  // begin, count, req, rb      [4][n_seg_cap]
   DevBuf n_items, items, order, pm, pl, po, a_rows;
+  DevBuf unit_ctr;  // attention work counters [8], zero between launches
   DevBuf logits_ws, row_out;  // sampled verification: full logits, per-row outcomes
   DevBuf tree_i32;            // tree drafts: kvpos, tmask [2][max_rows]
   DevBuf path_ws;             // tree drafts: accepted path when the caller passes none
@@ -365,6 +366,7 @@ AttnArgs attn_args(war_model* m, war_kv_pool* p, int TB, int chunk) {
   a.pl = m->pl.as<float>();
   a.po = m->po.as<float>();
   a.o = m->o.as<bf16_t>();
+  a.unit_ctr = m->unit_ctr.as<int32_t>();
   return a;
 }
 
@@ -509,6 +511,8 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
   ok(m->segs_i32.ensure((size_t)4 * m->n_seg_cap * 4));
   ok(m->n_items.ensure(16));
   ok(m->a_rows.ensure((size_t)kMaxBatch * 4));
+  ok(m->unit_ctr.ensure(8 * 4));
+  if (e == hipSuccess) e = hipMemset(m->unit_ctr.p, 0, m->unit_ctr.bytes);
   if (e == hipSuccess) {
     std::vector<double> inv(md.hd / 2);
     for (int j = 0; j < md.hd / 2; ++j) inv[j] = std::pow((double)cfg->rope_base, -2.0 * j / md.hd);
@@ -526,7 +530,7 @@ void war_model_destroy(war_model* m) {
   if (!m) return;
   for (DevBuf* b : {&m->wts, &m->h, &m->u, &m->q, &m->o, &m->y, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
                     &m->amax_v, &m->amax_i, &m->rows_i32, &m->tree_i32, &m->path_ws, &m->reqs_i32, &m->segs_i32, &m->n_items,
-                    &m->items, &m->order, &m->logits_ws, &m->row_out, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
+                    &m->items, &m->order, &m->unit_ctr, &m->logits_ws, &m->row_out, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
     b->release();
   if (m->pinned) (void)hipHostFree(m->pinned);
   for (hipEvent_t e : m->prof.pool) (void)hipEventDestroy(e);
