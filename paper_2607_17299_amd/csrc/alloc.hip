@@ -108,6 +108,7 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
   __shared__ int s_fail;
   __shared__ int s_ctx[kBT], s_dl[kBT];
   __shared__ int s_pg0[kBT], s_nch[kBT], s_seq[kBT], s_shr[kBT], s_noff[kBT], s_run[kBT];
+  __shared__ int s_lead[kBT], s_np[kBT], s_mis[kBT];
   const int t = threadIdx.x;
   const int kp1 = a.k_max + 1;
   __shared__ int s_bad;
@@ -181,15 +182,23 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
       regular = regular && s_nch[L + g] == s_nch[L];
       ++g;
     }
-    if (g > 1 && nch > 0) {
-      const int np = min(s_ctx[t], s_ctx[L]) / p.page_size;
-      const int32_t* rb = p.table + (int64_t)s_seq[t] * p.max_pages;
-      const int32_t* rl = p.table + (int64_t)s_seq[L] * p.max_pages;
-      int c = 0;
-      while (c < np && rb[c] == rl[c]) ++c;
-      atomicMin(&s_shr[L], c * p.page_size);
-    }
+    s_lead[t] = L;
+    s_np[t] = (g > 1 && nch > 0) ? min(s_ctx[t], s_ctx[L]) / p.page_size : -1;
+    s_mis[t] = max(s_np[t], 0);
   }
+  __syncthreads();
+  // first page (below np) where a member's block table differs from the first
+  // member's: all threads compare one request's pages at a time
+  for (int q = 0; q < a.B; ++q) {
+    const int np = s_np[q];
+    if (np <= 0) continue;
+    const int32_t* rb = p.table + (int64_t)s_seq[q] * p.max_pages;
+    const int32_t* rl = p.table + (int64_t)s_seq[s_lead[q]] * p.max_pages;
+    for (int c = t; c < np; c += kBT)
+      if (rb[c] != rl[c]) atomicMin(&s_mis[q], c);
+  }
+  __syncthreads();
+  if (t < a.B && s_np[t] >= 0) atomicMin(&s_shr[L], s_mis[t] * p.page_size);
   __syncthreads();
   // Shared-prefix units: the whole attention chunks a group shares are attended
   // once per run of consecutive members whose live rows (G per token) fit one
