@@ -8,10 +8,14 @@ head_dim 128, FFN 12288, vocab 151936).
 * Prefill-append on the same shapes, then a verify step on the appended KV.
 * The multi-turn append path: forked shared prefixes, an appended observation,
   then a k = 4 verify step.
-* The full 36-layer low-load workload exactly as the benchmark runs it (8 x
-  32768 cached tokens, k = 8), checked on a sampled request.
+* The full 36-layer workloads exactly as the benchmark runs them, checked on
+  sampled requests: low load (8 x 32768 cached tokens, k = 8), high load (64
+  lognormal contexts, k = 0 and k = 2) and multi-turn (forked prefixes, a
+  2048-token append, then k = 4).
 The cached contexts come from the seeded generator (an input of the step), so
-the oracle reads the very same keys and values.
+the oracle reads the very same keys and values; after the multi-turn append
+the oracle reads the cached keys and values back from the pool (the append's
+own parity is checked at reduced depth).
 """
 import numpy as np
 import pytest
@@ -315,16 +319,21 @@ def _oracle_kv_stream(cfg, kv_seed, seq, ctx, tag):
     return kv_get
 
 
-def _full_size_check(st, kv_seed, sample, tag):
+def _full_size_check(st, kv_seed, sample, tag, setup=None):
     """Run one verify step of the 36-layer model on the GPU with logits and
     recompute the sampled requests with the oracle (float64, and its fp32-
-    accumulation mode for the tolerance), layer by layer."""
+    accumulation mode for the tolerance), layer by layer.  `setup`, when given,
+    builds (model, pool, step, kv_get factory) instead of the seeded contexts."""
     war = _war()
     cfg = synth.LARGE
     w = harness.large_weights(cfg)
-    model = war.Model(cfg, w, max_rows=1024)
-    pool = harness.make_pool(cfg, st.ctx_lens, max(st.k_max, 2) + 8)
-    harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, kv_seed)
+    if setup is None:
+        model = war.Model(cfg, w, max_rows=1024)
+        pool = harness.make_pool(cfg, st.ctx_lens, max(st.k_max, 2) + 8)
+        harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, kv_seed)
+        kv_source = lambda b, ctx: _oracle_kv_stream(cfg, kv_seed, int(st.seq_ids[b]), ctx, f"{tag} req {b}")
+    else:
+        model, pool, st, kv_source = setup(war, cfg, w)
     ds = harness.DeviceStep(st, with_logits=True, vocab=cfg.vocab)
     ds.verify(model, pool, logits=True)
     ds.commit(pool, discard=False)
@@ -337,7 +346,7 @@ def _full_size_check(st, kv_seed, sample, tag):
     report, out = [], []
     for b in sample:
         ctx = int(st.ctx_lens[b])
-        kv_get = _oracle_kv_stream(cfg, kv_seed, int(st.seq_ids[b]), ctx, f"{tag} req {b}")
+        kv_get = kv_source(b, ctx)
         tokens = [int(st.last_tokens[b])] + list(st.drafts[b])
         o64, _ = forward_block(cfg, W, tokens, ctx, kv_get)
         o32, _ = forward_block(cfg, W, tokens, ctx, kv_get, precision="fp32")
@@ -354,6 +363,45 @@ def test_full_size_low_load_sampled():
     """The benchmark's workload at full size (36 layers, 8 x 32768, k = 8);
     request 0 is recomputed by the oracle."""
     _full_size_check(harness.low_load_step(), 5, [0], "low_load")
+
+
+def test_full_size_high_load_sampled():
+    """64 requests with lognormal contexts and k = 0 (plain batched decode);
+    the shortest and the longest request are recomputed by the oracle."""
+    st = harness.high_load_step(k=0)
+    sample = [int(np.argmin(st.ctx_lens)), int(np.argmax(st.ctx_lens))]
+    _full_size_check(st, 5, sample, "high_load")
+
+
+def test_full_size_multi_turn_sampled():
+    """16 trajectories in 4 groups sharing a forked 8192-token prefix (24576
+    cached tokens each), a 2048-token observation appended to each with
+    war_prefill_append, then the k = 4 verify step (shared-prefix attention
+    units).  Trajectories 0 and 5 (two groups) are recomputed by the oracle
+    from the cached keys and values the pool holds after the append."""
+    def setup(war, cfg, w):
+        model = war.Model(cfg, w, max_rows=1024)
+        mt = harness.multi_turn_inputs(vocab=cfg.vocab)
+        pool = harness.multi_turn_pool(cfg, mt, 4)
+        harness.load_multi_turn(pool, cfg, mt, 5)
+        nxt, ctx_dev, _ = harness.multi_turn_append(model, pool, mt)
+        torch.cuda.synchronize()
+        assert ctx_dev.cpu().tolist() == [mt.cached + mt.n_new] * mt.n
+        st = harness.multi_turn_step(mt, nxt.cpu().numpy(), 4)
+
+        def kv_source(b, ctx):
+            cache = {}
+
+            def kv_get(l):
+                if l not in cache:
+                    print(f"multi_turn traj {b}: oracle layer {l}", flush=True)
+                    a = pool.gather_kv(int(st.seq_ids[b]), ctx, l).cpu().double().numpy()
+                    cache.clear()
+                    cache[l] = (a[0], a[1])
+                return cache[l]
+            return kv_get
+        return model, pool, st, kv_source
+    _full_size_check(None, 5, [0, 5], "multi_turn", setup=setup)
 
 
 def test_full_size_high_load_k2_sampled():
