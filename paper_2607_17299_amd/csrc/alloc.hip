@@ -237,13 +237,20 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
   // chunk at the same time, so later readers find it in cache); otherwise
   // request order, a run's shared units first.
   if (t < a.B && nch > 0) {
+    // slot o of the order gets chunk c of this request (and its descriptor)
+    auto put = [&](int o, int c) {
+      m.order[o] = ioff + c;
+      const int wc = c < nsc ? (run > 0 ? run : -1) : 0;
+      m.udesc[2 * o] = make_int4(ioff + c, t, c, (dl + 1) << 16);  // first token 0, dl + 1 rows' tokens
+      m.udesc[2 * o + 1] = make_int4(wc, s, ctx, t * kp1);
+    };
     if (nsc == 0 && g > 1 && regular) {
-      for (int c = 0; c < nch; ++c) m.order[s_noff[L] + c * g + j] = ioff + c;
+      for (int c = 0; c < nch; ++c) put(s_noff[L] + c * g + j, c);
     } else {
       int o = noff;
       if (run > 0)
-        for (int c = 0; c < nsc; ++c) m.order[o++] = ioff + c;
-      for (int c = nsc; c < nch; ++c) m.order[o++] = ioff + c;
+        for (int c = 0; c < nsc; ++c) put(o++, c);
+      for (int c = nsc; c < nch; ++c) put(o++, c);
     }
   }
   if (t == 0) {

@@ -66,7 +66,7 @@ k_attn(AttnArgs a) {
   // the wave index is wave-uniform: block positions, page ids and page bases
   // derived from it live in scalar registers
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int total = (a.meta.order ? a.meta.n_items[1] : a.meta.n_items[0]) * a.n_kv_heads;
+  const int total = a.meta.n_items[1] * a.n_kv_heads;  // units: work-order slots x kv-heads
   const int P = a.kv.page_size;
   // key row of this lane in S^T tile t (within a 32-key block); tile 1 adds 4
   const int kk0 = (ln >> 2) * 8 + (ln & 3);
@@ -84,28 +84,29 @@ k_attn(AttnArgs a) {
   // runs on the same XCD, and items that are neighbours in the work order (the
   // same prefix chunk of sibling requests) share its L2.  The combine kernel
   // that follows every launch resets the counters.
+  //
+  // The next unit is taken from the counter when the key loop of the current
+  // one ends, so the counter's latency overlaps the merge; a unit starts with
+  // one (scalar) load of its work-order slot's descriptor instead of a chain
+  // of dependent loads (order, item, request fields).
   const int NC = min(8, (int)gridDim.x);
   const int cls = blockIdx.x % NC;
-  __shared__ int s_next;
+  __shared__ int s_it;
+  if (tid == 0) s_it = atomicAdd(&a.unit_ctr[cls], 1) * NC + cls;
+  __syncthreads();
   for (;;) {
-    if (tid == 0) s_next = atomicAdd(&a.unit_ctr[cls], 1);
-    __syncthreads();
-    // (the loop body passes a barrier before thread 0 rewrites s_next)
-    const int it = s_next * NC + cls;
+    const int it = s_it;
     if (it >= total) break;
-    // units in work order
-    const int slot = it / a.n_kv_heads, kvh = it % a.n_kv_heads;
-    const int item = a.meta.order ? a.meta.order[slot] : slot;
-    const int4 itm = a.meta.items[item];
-    const int b = itm.x, t0 = itm.y * a.TB, chunk = itm.z;
+    const int kvh = it % a.n_kv_heads;
+    const int4 u0 = a.meta.udesc[2 * (it / a.n_kv_heads)], u1 = a.meta.udesc[2 * (it / a.n_kv_heads) + 1];
+    const int item = u0.x, b = u0.y, chunk = u0.z;
+    const int t0 = u0.w & 0xffff, nt = u0.w >> 16;
     // a shared-prefix unit (.w = n > 0) covers the live rows of requests
     // b .. b+n-1, one after the other, and sees every key of its chunk (the
     // shared keys precede every member's rows): no causal mask
-    const bool shared = itm.w > 0;
-    const int nmem = shared ? itm.w : 1;
-    const int seq = a.meta.req_seq[b], pos0 = a.meta.req_pos0[b];
-    const int row0 = a.meta.req_row0[b];
-    const int nt = min(a.TB, a.meta.req_ntok[b] - t0);
+    const bool shared = u1.x > 0;
+    const int nmem = shared ? u1.x : 1;
+    const int seq = u1.y, pos0 = u1.z, row0 = u1.w;
     int nrows = nt * a.G;
     if (shared)
       for (int jm = 1; jm < nmem; ++jm) nrows += min(a.TB, a.meta.req_ntok[b + jm]) * a.G;
@@ -367,6 +368,10 @@ k_attn(AttnArgs a) {
       }
     }
 
+    // the next unit: the counter's reply arrives during the merge
+    int next_it = 0;
+    if (tid == 0) next_it = atomicAdd(&a.unit_ctr[cls], 1) * NC + cls;
+
     // ---- merge the 4 waves (fixed order) and write the item's partial
 #pragma unroll
     for (int rt = 0; rt < NR; ++rt) {
@@ -425,6 +430,8 @@ k_attn(AttnArgs a) {
         a.pl[prow] = l;
       }
     }
+    // every thread has read s_it at the top of this unit (the merge passed barriers)
+    if (tid == 0) s_it = next_it;
     __syncthreads();
   }
 }

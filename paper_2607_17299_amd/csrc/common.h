@@ -93,6 +93,10 @@ struct StepMeta {
   // .w > 0 is a shared-prefix unit covering the rows of requests x .. x+w-1.
   int32_t* order;
   int32_t* n_items;     // [0] item slots, [1] units in the work order
+  // the work order resolved: per slot of the order, two int4
+  //   (item, request, key chunk, first token | rows' token count << 16),
+  //   (.w of the item, sequence id, request position 0, request's first row)
+  int4* udesc;
   int32_t* seg_begin;   // [n_segs]
   int32_t* seg_count;   // [n_segs]
   int32_t* seg_req;     // [n_segs]

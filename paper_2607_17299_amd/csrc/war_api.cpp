@@ -105,7 +105,7 @@ struct war_model {
   DevBuf rows_i32;  // tok, pos, active, row_req  [4][max_rows]
   DevBuf reqs_i32;  // seq, pos0, ntok, row0      [4][n_req_cap]
   DevBuf segs_i32;  // begin, count, req, rb      [4][n_seg_cap]
-  DevBuf n_items, items, order, pm, pl, po, a_rows;
+  DevBuf n_items, items, order, udesc, pm, pl, po, a_rows;
   DevBuf unit_ctr;  // attention work counters [8], zero between launches
   DevBuf logits_ws, row_out;  // sampled verification: full logits, per-row outcomes
   DevBuf tree_i32;            // tree drafts: kvpos, tmask [2][max_rows]
@@ -131,6 +131,7 @@ struct war_model {
     m.req_ntok = q4 + 2 * n_req_cap;
     m.req_row0 = q4 + 3 * n_req_cap;
     m.items = items.as<int4>();
+    m.udesc = udesc.as<int4>();
     m.order = order.as<int32_t>();
     m.n_items = n_items.as<int32_t>();
     int32_t* s4 = segs_i32.as<int32_t>();
@@ -372,6 +373,7 @@ AttnArgs attn_args(war_model* m, war_kv_pool* p, int TB, int chunk) {
 
 war_status ensure_items(war_model* m, int64_t n_items, int RB) {
   HIPCHK(m->items.ensure(std::max<int64_t>(n_items, 1) * sizeof(int4)));
+  HIPCHK(m->udesc.ensure(std::max<int64_t>(n_items, 1) * 2 * sizeof(int4)));
   HIPCHK(m->order.ensure(std::max<int64_t>(n_items, 1) * sizeof(int32_t)));
   const int64_t pr = std::max<int64_t>(n_items, 1) * m->md.nkv * RB;
   HIPCHK(m->pm.ensure(pr * sizeof(float)));
@@ -530,7 +532,7 @@ void war_model_destroy(war_model* m) {
   if (!m) return;
   for (DevBuf* b : {&m->wts, &m->h, &m->u, &m->q, &m->o, &m->y, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
                     &m->amax_v, &m->amax_i, &m->rows_i32, &m->tree_i32, &m->path_ws, &m->reqs_i32, &m->segs_i32, &m->n_items,
-                    &m->items, &m->order, &m->unit_ctr, &m->logits_ws, &m->row_out, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
+                    &m->items, &m->order, &m->udesc, &m->unit_ctr, &m->logits_ws, &m->row_out, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
     b->release();
   if (m->pinned) (void)hipHostFree(m->pinned);
   for (hipEvent_t e : m->prof.pool) (void)hipEventDestroy(e);
@@ -976,7 +978,7 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
     const int nr = (int)rq_seq.size();
     std::vector<int32_t> pos(R), act(R, 1), rreq(R);
     std::vector<int32_t> sg_b, sg_c, sg_r, sg_rb;
-    std::vector<int4> items;
+    std::vector<int4> items, udesc;
     for (int j = 0; j < nr; ++j) {
       for (int t = 0; t < rq_ntok[j]; ++t) {
         pos[rq_row0[j] + t] = rq_pos0[j] + t;
@@ -989,7 +991,12 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
         sg_c.push_back(nch);
         sg_r.push_back(j);
         sg_rb.push_back(rb);
-        for (int c = 0; c < nch; ++c) items.push_back(make_int4(j, rb, c, 0));
+        const int t0 = rb * TB, ntk = std::min(TB, rq_ntok[j] - t0);
+        for (int c = 0; c < nch; ++c) {
+          udesc.push_back(make_int4((int)items.size(), j, c, t0 | (ntk << 16)));
+          udesc.push_back(make_int4(0, rq_seq[j], rq_pos0[j], rq_row0[j]));
+          items.push_back(make_int4(j, rb, c, 0));
+        }
       }
     }
     const int nseg = (int)sg_b.size();
@@ -1016,8 +1023,10 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
     HIPCHK(h2d(meta.seg_req, sg_r.data(), nseg * 4));
     HIPCHK(h2d(meta.seg_rb, sg_rb.data(), nseg * 4));
     HIPCHK(h2d(meta.items, items.data(), items.size() * sizeof(int4)));
-    const int32_t ni = (int32_t)items.size();
-    HIPCHK(h2d(meta.n_items, &ni, 4));
+    HIPCHK(h2d(meta.udesc, udesc.data(), udesc.size() * sizeof(int4)));
+    const int32_t ni2[2] = {(int32_t)items.size(), (int32_t)items.size()};  // prefill: the work order is the item list
+    const int32_t ni = ni2[0];
+    HIPCHK(h2d(meta.n_items, ni2, 8));
     HIPCHK(hipStreamSynchronize(st));  // host vectors go out of scope below
 
     AttnArgs a = attn_args(m, p, TB, chunk);
