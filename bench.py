@@ -65,6 +65,24 @@ def timed_steps(ds, model, pool, steps: int):
     return (time.perf_counter() - t0) * 1e3 / steps
 
 
+def step_distribution(ds, model, pool, steps: int):
+    """Per-step times (HIP events on the launch stream, one pair per step) in a
+    pass of its own after the timed steps: median, p10 and p90 in ms."""
+    import numpy as np
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for e0, e1 in ev:
+        e0.record()
+        ds.run(model, pool)
+        ds.commit(pool, discard=True)
+        e1.record()
+    torch.cuda.synchronize()
+    t = np.array([e0.elapsed_time(e1) for e0, e1 in ev])
+    return {"median": round(float(np.median(t)), 4), "p10": round(float(np.percentile(t, 10)), 4),
+            "p90": round(float(np.percentile(t, 90)), 4), "steps": steps}
+
+
 def kernel_profile(ds, model, pool, war, steps: int = 2):
     war.profile(model, True)
     for _ in range(steps):
@@ -270,6 +288,7 @@ def main():
     value = accepted / (ms / 1e3)
     log(f"{ms:.3f} ms/step, accept {acc.tolist()}")
 
+    dist = step_distribution(ds, model, pool, args.steps)
     prof = kernel_profile(ds, model, pool, war)
     attn = prof.get("attention", {"calls": 0, "ms": 0.0})
     per_launch_ms = attn["ms"] / max(attn["calls"], 1)
@@ -331,6 +350,10 @@ def main():
                                          "accepted_tokens_per_s": round(float((acc3 + 1).sum() / (ms3 / 1e3)), 1),
                                          "accept_lens": acc3.tolist()}
 
+    drafter = None
+    if args.workload == "low_load":
+        drafter = harness.time_low_load_drafter()
+
     cpu = None
     if not args.no_cpu_baseline:
         log("timing the oracle on the host")
@@ -353,6 +376,8 @@ def main():
         "hbm": {"step_bytes": total_bytes, "achieved_GBps": round(step_gbps, 1),
                 "frac_of_peak": round(step_gbps / HBM_PEAK_GBPS, 4)},
         "verified_positions_per_s": round(st.rows() / (ms / 1e3), 1),
+        "step_ms_events": dist,
+        "drafter_host": drafter,
         "accept_lens": acc.tolist(),
         "roofline": {"kernel": "attention (k_attn)", "bound": "hbm", "achieved": round(attn_gbps, 1),
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),

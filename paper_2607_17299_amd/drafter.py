@@ -42,7 +42,7 @@ class SuffixDrafter:
         self.max_match = max_match
         self._parts: List[np.ndarray] = []
         self._corpus = np.full(1, _SEP, dtype=np.int64)
-        self._dirty = False
+        self._dirty = True
 
     def add_trajectory(self, tokens: Sequence[int]) -> None:
         """External update interface: add one finished trajectory."""
@@ -55,14 +55,27 @@ class SuffixDrafter:
             for p in self._parts:
                 pieces += [p, np.full(1, _SEP, np.int64)]
             self._corpus = np.concatenate(pieces)
+            # token -> its positions (ascending), every position but the last:
+            # a stable sort groups equal tokens and keeps their order
+            head = self._corpus[:-1]
+            self._pos = np.argsort(head, kind="stable")
+            self._vals, self._start = np.unique(head[self._pos], return_index=True)
             self._dirty = False
+
+    def _positions(self, tok: int) -> np.ndarray:
+        """Ascending corpus positions (except the last) holding `tok`."""
+        i = int(np.searchsorted(self._vals, tok))
+        if i >= len(self._vals) or self._vals[i] != tok:
+            return np.zeros(0, np.int64)
+        end = self._start[i + 1] if i + 1 < len(self._vals) else len(self._pos)
+        return self._pos[self._start[i]:end]
 
     def _longest_match(self, pattern: np.ndarray) -> np.ndarray:
         """End positions (in the corpus) of the longest matching suffix, or empty."""
         c = self._corpus
         if len(pattern) == 0:
             return np.zeros(0, np.int64)
-        cand = np.nonzero(c[:-1] == pattern[-1])[0]     # must be followed by a position
+        cand = self._positions(int(pattern[-1]))         # must be followed by a position
         cand = cand[c[cand + 1] != _SEP]
         best = cand
         L = 1

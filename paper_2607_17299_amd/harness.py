@@ -175,6 +175,29 @@ def low_load_step(seed: int = 2, B: int = 8, ctx: int = 32768, k: int = 8, n_pri
     return Step(np.arange(B, dtype=np.int32), np.full(B, ctx, np.int32), last, drafts, k)
 
 
+def time_low_load_drafter(seed: int = 2, B: int = 8, ctx: int = 32768, k: int = 8, n_prior: int = 64,
+                          vocab: int = 151936, reps: int = 5) -> dict:
+    """Host cost of the low-load drafts (the suffix drafter is harness logic,
+    outside the verify step): building the index over the prior trajectories
+    once, and proposing k drafts for the B requests (median of `reps`)."""
+    import time
+    contexts, prior = low_load_tokens(seed, B, ctx, n_prior, ctx, vocab)
+    d = SuffixDrafter()
+    for p in prior:
+        d.add_trajectory(p)
+    t0 = time.perf_counter()
+    d._build()
+    build_ms = (time.perf_counter() - t0) * 1e3
+    times = []
+    for _ in range(reps):
+        t0 = time.perf_counter()
+        for b in range(B):
+            d.propose(contexts[b], k)
+        times.append((time.perf_counter() - t0) * 1e3)
+    return {"index_build_ms": round(build_ms, 2), "propose_batch_ms": round(float(np.median(times)), 3),
+            "corpus_tokens": int(sum(len(p) for p in prior)), "requests": B, "k": k}
+
+
 def diverging_siblings(cont: List[List[int]], seed: int, vocab: int) -> List[List[List[int]]]:
     """Three sibling continuations per request, added in this order: one that
     leaves the target's continuation at its first token, one that leaves it at
