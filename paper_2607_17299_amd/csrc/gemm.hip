@@ -8,14 +8,17 @@
 // Weights are repacked once, when the model is created, into MFMA fragment
 // order: for n-tile nt (16 output rows), k-step s (64 inputs) and half j, the
 // 1 KB fragment holds, for lane l, the 8 values
-//     W[nt*16 + l%16][s*64 + (l/16)*16 + j*8 + e],  e = 0..7,
-// and fragments are stored nt-major, then s, then j.  One wave-wide 16-byte
-// load then reads 1 KB of contiguous memory, and a wave walking k for one
-// n-tile streams a contiguous run (2 KB per step) -- the HBM-friendly pattern
-// of a plain copy, where row-major W would touch 16 rows 8-24 KB apart per load.
+//     W[nt*16 + l%16][s*64 + (l/16)*16 + j*8 + e],  e = 0..7.
+// The 8 n-tiles of one workgroup form a group; a group's fragments are stored
+// step-major: step s, then tile t (0..7), then half j.  A workgroup then reads
+// one contiguous 16 KB piece per k-step and its whole slice of W as a single
+// run, the access pattern of a plain copy (row-major W would touch 16 rows
+// 8-24 KB apart per load).  For the stacked [gate; up] matrix, group g holds
+// gate tiles 4g..4g+3 as t = 0..3 and the matching up tiles as t = 4..7.
 //
 // Workgroup = 4 waves = 128 output columns; each wave owns 32 columns (two
-// 16-wide MFMA n-tiles) and all MT 16-row m-tiles of the workgroup's m-block.
+// 16-wide MFMA n-tiles: t = 2w, 2w+1, or gate t = w and up t = w + 4) and all
+// MT 16-row m-tiles of the workgroup's m-block.
 // K advances in steps of 64:
 //   * W goes straight from HBM to registers (4 fragments per wave and step);
 //   * the A tile (MT*16 rows x 64) is loaded into registers by all 256 threads
@@ -31,9 +34,9 @@
 // P[split][M][N] and a row kernel adds them in a fixed order (deterministic).
 // The argmax epilogue (LM head, one split) writes optional fp32 logits and the
 // best (value, lowest index) of each row within each 128-column block.  The
-// SwiGLU epilogue (gate/up, one split) takes the [gate; up] matrix with wave w
-// of block nb owning gate n-tile 4nb + w and the matching up n-tile, and
-// writes bf16 silu(gate) * up for its 16 columns.
+// SwiGLU epilogue (gate/up, one split) takes the paired [gate; up] groups,
+// wave w of block nb owning gate n-tile 4nb + w and the matching up n-tile,
+// and writes bf16 silu(gate) * up for its 16 columns.
 #include "kernels.h"
 
 namespace {
@@ -80,10 +83,9 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
   const int nsteps = NSTEPS > 0 ? NSTEPS : (ke - kb) / KS;
   const int n0 = nb * 128;
   const int S = g.K / KS;  // k-steps per n-tile in the packed layout
-  // first n-tile of the block: 8 consecutive tiles, or (SwiGLU) 4 gate tiles
-  // whose up tiles sit N/32 tiles further on
-  const int tb = EPI == EPI_SWIGLU ? nb * 4 : nb * 8;
-  const bf16_t* Wb = g.Wp + (int64_t)tb * S * (KS * 16);
+  // SwiGLU: the block's first gate tile (output column tile of the epilogue)
+  const int tb = nb * 4;
+  const bf16_t* Wb = g.Wp + (int64_t)nb * S * (8 * KS * 16);
 
   // Loads are raw buffer loads (one descriptor for the W block, one for A): the
   // compiler does not re-issue them next to their use, so they stay in flight
@@ -95,9 +97,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(Wb), 0, 0x7fffffff, 0x00020000);
   const __amdgpu_buffer_rsrc_t ares =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(g.A), 0, 0x7fffffff, 0x00020000);
-  // byte offsets of this lane's fragments of step 0 (n-tiles 2w and 2w+1)
-  const int wv0 = ((EPI == EPI_SWIGLU ? w : w * 2) * S + kb / KS) * (KS * 32) + lane * 16;
-  const int wv1 = wv0 + (EPI == EPI_SWIGLU ? g.N / 32 : 1) * S * (KS * 32);
+  // byte offsets of this lane's fragments of the split's first step (tiles
+  // 2w and 2w+1, or gate tile w and up tile w + 4); a step is 16 KB further
+  const int wv0 = ((kb / KS) * 8 + (EPI == EPI_SWIGLU ? w : w * 2)) * (KS * 32) + lane * 16;
+  const int wv1 = wv0 + (EPI == EPI_SWIGLU ? 4 : 1) * (KS * 32);
   int av[Tile<MT>::PER_THREAD];
   int aoff[Tile<MT>::PER_THREAD];
 #pragma unroll
@@ -114,10 +117,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
   };
   auto load_w = [&](uint4* wr, int s) {
-    wr[0] = bload(wres, wv0, s * KS * 32);
-    wr[1] = bload(wres, wv0 + 1024, s * KS * 32);
-    wr[2] = bload(wres, wv1, s * KS * 32);
-    wr[3] = bload(wres, wv1 + 1024, s * KS * 32);
+    wr[0] = bload(wres, wv0, s * KS * 256);
+    wr[1] = bload(wres, wv0 + 1024, s * KS * 256);
+    wr[2] = bload(wres, wv1, s * KS * 256);
+    wr[3] = bload(wres, wv1 + 1024, s * KS * 256);
   };
   auto load_a = [&](uint4* ar, int s) {
 #pragma unroll
@@ -293,29 +296,34 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   }
 }
 
-// One 16-byte fragment chunk per thread: chunk c = ((nt * S + s) * 2 + j) * 64 + l.
-__global__ void k_pack_weights(const bf16_t* __restrict__ W, int K, int64_t chunks,
-                               uint4* __restrict__ dst) {
+// One 16-byte fragment chunk per thread: chunk c = (((g * S + s) * 8 + t) * 2 + j) * 64 + l
+// for tile t of group g; W2 non-null: t < 4 is tile 4g + t of W, t >= 4 tile
+// 4g + t - 4 of W2 (the gate/up pairing), else tile 8g + t of W.
+__global__ void k_pack_weights(const bf16_t* __restrict__ W, const bf16_t* __restrict__ W2, int K,
+                               int64_t chunks, uint4* __restrict__ dst) {
   const int S = K / KS;
   for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < chunks;
        c += (int64_t)gridDim.x * blockDim.x) {
     const int l = (int)(c & 63);
     const int j = (int)((c >> 6) & 1);
-    const int64_t ts = c >> 7;  // nt * S + s
-    const int64_t nt = ts / S;
-    const int s = (int)(ts - nt * S);
-    const int64_t row = nt * 16 + (l & 15);
+    const int t = (int)((c >> 7) & 7);
+    const int64_t gs = c >> 10;  // g * S + s
+    const int64_t grp = gs / S;
+    const int s = (int)(gs - grp * S);
+    const bf16_t* src = W2 && t >= 4 ? W2 : W;
+    const int64_t tile = W2 ? grp * 4 + (t & 3) : grp * 8 + t;
+    const int64_t row = tile * 16 + (l & 15);
     const int col = s * KS + (l >> 4) * 16 + j * 8;
-    dst[c] = *reinterpret_cast<const uint4*>(W + row * K + col);
+    dst[c] = *reinterpret_cast<const uint4*>(src + row * K + col);
   }
 }
 
 }  // namespace
 
-void launch_pack_weights(const bf16_t* W, int N, int K, bf16_t* dst, hipStream_t st) {
+void launch_pack_weights(const bf16_t* W, const bf16_t* W2, int N, int K, bf16_t* dst, hipStream_t st) {
   const int64_t chunks = (int64_t)N * K / 8;
   const int blocks = (int)std::min<int64_t>((chunks + 255) / 256, 16384);
-  k_pack_weights<<<blocks, 256, 0, st>>>(W, K, chunks, reinterpret_cast<uint4*>(dst));
+  k_pack_weights<<<blocks, 256, 0, st>>>(W, W2, K, chunks, reinterpret_cast<uint4*>(dst));
 }
 
 // 16-row tiles per workgroup: up to 6 (96 rows); more rows take more m-blocks

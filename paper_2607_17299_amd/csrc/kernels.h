@@ -89,7 +89,10 @@ void launch_add_ctx(int n, int32_t* ctx, const int32_t* add, hipStream_t st);
 int gemm_mt(int M);  // 16-row tiles per workgroup for M rows
 void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st);
 // W [N][K] row-major -> dst in MFMA fragment order; N % 16 == 0, K % 64 == 0
-void launch_pack_weights(const bf16_t* W, int N, int K, bf16_t* dst, hipStream_t st);
+// Repack [N][K] weights (N % 128 == 0) into the GEMM's grouped fragment order;
+// W2 non-null: W and W2 are the gate and up halves ([N/2][K] each) of a SwiGLU
+// pair, interleaved in groups of 4 + 4 tiles.
+void launch_pack_weights(const bf16_t* W, const bf16_t* W2, int N, int K, bf16_t* dst, hipStream_t st);
 
 // sampled verification (sample.hip)
 struct SampleArgs {
@@ -125,7 +128,6 @@ void launch_qkv_rope(int rows, int splits, const float* P, const ModelDims& md,
                      const float* cos_t, const float* sin_t, const StepMeta& meta,
                      const int32_t* row_req, const int32_t* table, int max_pages, const KvGeom& kv,
                      int layer, bf16_t* q, hipStream_t st);
-void launch_swiglu(int rows, int splits, const float* P, int F, bf16_t* y, hipStream_t st);
 // parents (nullable): tree drafts; accept_path [n_req][k_max] then receives the
 // accepted nodes in depth order, -1 beyond the accept length
 void launch_argmax_accept(int n_req, const int32_t* ntok, int row_stride, int n_blocks,

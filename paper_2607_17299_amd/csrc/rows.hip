@@ -168,25 +168,6 @@ __global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const fl
   }
 }
 
-// y = bf16(silu(gate) * up); gate = columns [0, F), up = [F, 2F) of the partials
-__global__ void __launch_bounds__(256) k_swiglu(int rows, int splits, const float* P, int F,
-                                                bf16_t* y) {
-  const int r = blockIdx.x;
-  const int c = (blockIdx.y * blockDim.x + threadIdx.x) * 4;
-  if (c >= F) return;
-  const int64_t N = 2 * (int64_t)F;
-  const int64_t sstride = (int64_t)rows * N;
-  const float* ps = P + (int64_t)r * N + c;
-  const float4 z = {0.f, 0.f, 0.f, 0.f};
-  const float4 gt = sum_splits(ps, sstride, splits, z);
-  const float4 up = sum_splits(ps + F, sstride, splits, z);
-  auto sw = [](float a, float b) { return a / (1.f + expf(-a)) * b; };
-  uint2 o;
-  o.x = pack2(sw(gt.x, up.x), sw(gt.y, up.y));
-  o.y = pack2(sw(gt.z, up.z), sw(gt.w, up.w));
-  *reinterpret_cast<uint2*>(y + (int64_t)r * F + c) = o;
-}
-
 // Per request: greedy token of each active row (best over the LM head's column
 // blocks, ties -> lowest id), then the acceptance.  Chain drafts: the longest
 // draft prefix that matches.  Tree drafts: a node is accepted when its parent
@@ -327,10 +308,6 @@ void launch_qkv_rope(int rows, int splits, const float* P, const ModelDims& md,
   dim3 grid(rows, cdiv_i(md.qkv / 2, 256));
   k_qkv_rope<<<grid, 256, 0, st>>>(rows, splits, P, md, cos_t, sin_t, meta, row_req, table,
                                    max_pages, kv, layer, q);
-}
-void launch_swiglu(int rows, int splits, const float* P, int F, bf16_t* y, hipStream_t st) {
-  dim3 grid(rows, cdiv_i(F / 4, 256));
-  k_swiglu<<<grid, 256, 0, st>>>(rows, splits, P, F, y);
 }
 void launch_argmax_accept(int n_req, const int32_t* ntok, int row_stride, int n_blocks,
                           const float* amax_v, const int32_t* amax_i, const int32_t* draft_tokens,

@@ -261,11 +261,11 @@ war_status gemm(war_model* m, const bf16_t* A, int lda, const int32_t* a_rows, c
   g.M = M;
   g.N = N;
   g.K = K;
+  // the paired gate/up layout is only read by the SwiGLU epilogue: one split
   Split sp{1, K};
-  if (!argmax) sp = pick_split(M, N, K, (int64_t)(m->P.bytes / 4));
+  if (!argmax && !swiglu_out) sp = pick_split(M, N, K, (int64_t)(m->P.bytes / 4));
   g.kper = sp.kper;
-  // SwiGLU in the epilogue when one split covers K (else the caller reduces)
-  const bool fuse = swiglu_out && sp.s == 1;
+  const bool fuse = swiglu_out != nullptr;
   g.out = swiglu_out;
   g.ld_out = N / 2;
   g.P = m->P.as<float>();
@@ -274,7 +274,6 @@ war_status gemm(war_model* m, const bf16_t* A, int lda, const int32_t* a_rows, c
   g.amax_v = m->amax_v.as<float>();
   g.amax_i = m->amax_i.as<int32_t>();
   launch_gemm(g, argmax ? EPI_ARGMAX : fuse ? EPI_SWIGLU : EPI_PARTIAL, sp.s, st);
-  if (swiglu_out && !fuse) launch_swiglu(M, sp.s, g.P, N / 2, swiglu_out, st);
   if (splits_out) *splits_out = sp.s;
   return WAR_OK;
 }
@@ -464,8 +463,16 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
   };
   auto pack = [&](int64_t N, int64_t K) {
     bf16_t* at = dst;
-    launch_pack_weights(src(), (int)N, (int)K, at, nullptr);
+    launch_pack_weights(src(), nullptr, (int)N, (int)K, at, nullptr);
     dst += N * K;
+    return at;
+  };
+  auto pack_pair = [&](int64_t F2, int64_t K) {  // gate [F2][K], then up [F2][K]
+    bf16_t* at = dst;
+    const bf16_t* gate = src();
+    const bf16_t* up = src();
+    launch_pack_weights(gate, up, (int)(2 * F2), (int)K, at, nullptr);
+    dst += 2 * F2 * K;
     return at;
   };
   m->embed = copy(V * d);
@@ -475,8 +482,7 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
     L.w_qkv = pack(md.qkv, d);
     L.w_o = pack(d, nqhd);
     L.ffn_norm = copy(d);
-    L.w_gate_up = pack(F, d);  // gate rows, then
-    pack(F, d);                // up rows directly after them
+    L.w_gate_up = pack_pair(F, d);
     L.w_down = pack(d, F);
     m->layers.push_back(L);
   }
