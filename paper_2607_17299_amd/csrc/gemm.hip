@@ -9,12 +9,15 @@
 // order: for n-tile nt (16 output rows), k-step s (64 inputs) and half j, the
 // 1 KB fragment holds, for lane l, the 8 values
 //     W[nt*16 + l%16][s*64 + (l/16)*16 + j*8 + e],  e = 0..7.
-// The 8 n-tiles of one workgroup form a group; a group's fragments are stored
-// step-major: step s, then tile t (0..7), then half j.  A workgroup then reads
-// one contiguous 16 KB piece per k-step and its whole slice of W as a single
-// run, the access pattern of a plain copy (row-major W would touch 16 rows
-// 8-24 KB apart per load).  For the stacked [gate; up] matrix, group g holds
-// gate tiles 4g..4g+3 as t = 0..3 and the matching up tiles as t = 4..7.
+// The 8 n-tiles of one workgroup form a group (16 KB per k-step), and the
+// whole matrix is stored step-major: k-step s, then group g, then tile t
+// (0..7), then half j.  A workgroup reads one contiguous 16 KB piece per
+// k-step, and the workgroups of a split, which advance through k together,
+// sweep one contiguous window of N/128 pieces: the access pattern of a plain
+// copy.  (Row-major W would touch 16 rows 8-24 KB apart per load; one run per
+// group, 16 KB per step, streamed 6-9% slower.)  For the stacked [gate; up]
+// matrix, group g holds gate tiles 4g..4g+3 as t = 0..3 and the matching up
+// tiles as t = 4..7.
 //
 // Workgroup = 4 waves = 128 output columns; each wave owns 32 columns (two
 // 16-wide MFMA n-tiles: t = 2w, 2w+1, or gate t = w and up t = w + 4) and all
@@ -82,10 +85,10 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
   const int ke = min(g.K, kb + g.kper);
   const int nsteps = NSTEPS > 0 ? NSTEPS : (ke - kb) / KS;
   const int n0 = nb * 128;
-  const int S = g.K / KS;  // k-steps per n-tile in the packed layout
   // SwiGLU: the block's first gate tile (output column tile of the epilogue)
   const int tb = nb * 4;
-  const bf16_t* Wb = g.Wp + (int64_t)nb * S * (8 * KS * 16);
+  const bf16_t* Wb = g.Wp + (int64_t)nb * (8 * KS * 16);
+  const int NG = g.N / 128;  // groups; one k-step of all groups is contiguous
 
   // Loads are raw buffer loads (one descriptor for the W block, one for A): the
   // compiler does not re-issue them next to their use, so they stay in flight
@@ -99,7 +102,9 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(g.A), 0, 0x7fffffff, 0x00020000);
   // byte offsets of this lane's fragments of the split's first step (tiles
   // 2w and 2w+1, or gate tile w and up tile w + 4); a step is 16 KB further
-  const int wv0 = ((kb / KS) * 8 + (EPI == EPI_SWIGLU ? w : w * 2)) * (KS * 32) + lane * 16;
+  const int wv0 = (EPI == EPI_SWIGLU ? w : w * 2) * (KS * 32) + lane * 16;
+  const int64_t sstride = (int64_t)NG * (KS * 256);  // bytes per k-step of the matrix
+  const int s0 = kb / KS;
   const int wv1 = wv0 + (EPI == EPI_SWIGLU ? 4 : 1) * (KS * 32);
   int av[Tile<MT>::PER_THREAD];
   int aoff[Tile<MT>::PER_THREAD];
@@ -117,10 +122,11 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
   };
   auto load_w = [&](uint4* wr, int s) {
-    wr[0] = bload(wres, wv0, s * KS * 256);
-    wr[1] = bload(wres, wv0 + 1024, s * KS * 256);
-    wr[2] = bload(wres, wv1, s * KS * 256);
-    wr[3] = bload(wres, wv1 + 1024, s * KS * 256);
+    const int so = (int)((s0 + s) * sstride);
+    wr[0] = bload(wres, wv0, so);
+    wr[1] = bload(wres, wv0 + 1024, so);
+    wr[2] = bload(wres, wv1, so);
+    wr[3] = bload(wres, wv1 + 1024, so);
   };
   auto load_a = [&](uint4* ar, int s) {
 #pragma unroll
@@ -296,20 +302,19 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   }
 }
 
-// One 16-byte fragment chunk per thread: chunk c = (((g * S + s) * 8 + t) * 2 + j) * 64 + l
-// for tile t of group g; W2 non-null: t < 4 is tile 4g + t of W, t >= 4 tile
+// One 16-byte fragment chunk per thread: chunk c = (((s * NG + g) * 8 + t) * 2 + j) * 64 + l
+// for tile t of group g (NG = N / 128 groups); W2 non-null: t < 4 is tile 4g + t of W, t >= 4 tile
 // 4g + t - 4 of W2 (the gate/up pairing), else tile 8g + t of W.
 __global__ void k_pack_weights(const bf16_t* __restrict__ W, const bf16_t* __restrict__ W2, int K,
-                               int64_t chunks, uint4* __restrict__ dst) {
-  const int S = K / KS;
+                               int64_t chunks, uint4* __restrict__ dst, int NG) {
   for (int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; c < chunks;
        c += (int64_t)gridDim.x * blockDim.x) {
     const int l = (int)(c & 63);
     const int j = (int)((c >> 6) & 1);
     const int t = (int)((c >> 7) & 7);
-    const int64_t gs = c >> 10;  // g * S + s
-    const int64_t grp = gs / S;
-    const int s = (int)(gs - grp * S);
+    const int64_t sg = c >> 10;  // s * NG + g
+    const int s = (int)(sg / NG);
+    const int64_t grp = sg - (int64_t)s * NG;
     const bf16_t* src = W2 && t >= 4 ? W2 : W;
     const int64_t tile = W2 ? grp * 4 + (t & 3) : grp * 8 + t;
     const int64_t row = tile * 16 + (l & 15);
@@ -323,7 +328,7 @@ __global__ void k_pack_weights(const bf16_t* __restrict__ W, const bf16_t* __res
 void launch_pack_weights(const bf16_t* W, const bf16_t* W2, int N, int K, bf16_t* dst, hipStream_t st) {
   const int64_t chunks = (int64_t)N * K / 8;
   const int blocks = (int)std::min<int64_t>((chunks + 255) / 256, 16384);
-  k_pack_weights<<<blocks, 256, 0, st>>>(W, W2, K, chunks, reinterpret_cast<uint4*>(dst));
+  k_pack_weights<<<blocks, 256, 0, st>>>(W, W2, K, chunks, reinterpret_cast<uint4*>(dst), N / 128);
 }
 
 // 16-row tiles per workgroup: up to 6 (96 rows); more rows take more m-blocks

@@ -185,6 +185,13 @@ war_status check_config(const war_model_config* c) {
   if (c->d_model % 128 || c->ffn_dim % 128 || c->vocab % 128 || qkv % 128 ||
       (c->n_q_heads * c->head_dim) % 128)
     return fail(WAR_ERR_UNSUPPORTED, "d_model, ffn_dim, vocab and projection widths must be multiples of 128");
+  {
+    // the GEMM addresses a packed matrix with 32-bit byte offsets
+    const int64_t d = c->d_model, big = std::max({(int64_t)c->vocab * d, 2 * (int64_t)c->ffn_dim * d,
+                                                   (int64_t)qkv * d, (int64_t)c->n_q_heads * c->head_dim * d});
+    if (big * 2 > 0x7fffffffLL - (1 << 16))
+      return fail(WAR_ERR_UNSUPPORTED, "a weight matrix of 2 GiB or more");
+  }
   if (c->head_dim != 64 && c->head_dim != 128) return fail(WAR_ERR_UNSUPPORTED, "head_dim must be 64 or 128");
   if (G > 8) return fail(WAR_ERR_UNSUPPORTED, "more than 8 query heads per kv head");
   if (c->page_size != 16) return fail(WAR_ERR_UNSUPPORTED, "page_size must be 16");
