@@ -154,8 +154,15 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
     m.req_ntok[t] = fail ? 0 : dl + 1;
     m.req_row0[t] = t * kp1;
   }
-  // attention items: chunks of the keys visible to the request's last row
-  const int nch = (t < a.B && !fail) ? cdiv_i(ctx + dl + 1, a.chunk) : 0;
+  // attention items: chunks of the keys visible to the request's last row.
+  // Longer chunks mean fewer partials to write and merge and fewer unit
+  // changes; they are used when the batch still has enough items for the grid
+  // and no sequences share pages (siblings that read a shared chunk at the same
+  // time find it in L2 more often when the chunks are short).
+  int n2;
+  (void)block_excl_scan((t < a.B && !fail) ? cdiv_i(ctx + dl + 1, 2 * a.chunk) : 0, sh, &n2);
+  const int chunk = n2 >= a.items_double && !a.cascade ? 2 * a.chunk : a.chunk;
+  const int nch = (t < a.B && !fail) ? cdiv_i(ctx + dl + 1, chunk) : 0;
   int n_items;
   const int ioff = block_excl_scan(nch, sh, &n_items);
   if (t < a.B) {
@@ -206,7 +213,7 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
   // member of a run owns it (item .w = members); the others' items for those
   // chunks are never scheduled (.w = -1).  Ordinary items keep .w = 0.
   const int RBs = a.rb;
-  if (t < a.B && a.cascade && L == t && g > 1 && nch > 0 && s_shr[t] >= a.chunk) {
+  if (t < a.B && a.cascade && L == t && g > 1 && nch > 0 && s_shr[t] >= chunk) {
     int j0 = 0, rows = 0;
     for (int jj = 0; jj < g; ++jj) {
       const int rj = a.G * (s_dl[t + jj] + 1);
@@ -222,7 +229,7 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
   }
   __syncthreads();
   int nsc = 0;
-  if (t < a.B && a.cascade && g > 1 && nch > 0 && s_shr[L] >= a.chunk) nsc = min(s_shr[L] / a.chunk, nch);
+  if (t < a.B && a.cascade && g > 1 && nch > 0 && s_shr[L] >= chunk) nsc = min(s_shr[L] / chunk, nch);
   const int j = t - L;
   const int run = nsc > 0 ? s_run[t] : 0;  // members of the run this request owns (0: not an owner)
   if (t < a.B && nsc > 0)
@@ -257,6 +264,7 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
     m.n_items[0] = n_items;
     m.n_items[1] = n_units;
     m.n_items[2] = 0;
+    m.n_items[3] = chunk;
     if (fail && !s_bad) p.scalars[1] |= ERR_NO_PAGES;
     if (!fail) p.scalars[0] = fc - total;
   }

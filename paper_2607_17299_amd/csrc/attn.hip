@@ -67,6 +67,7 @@ k_attn(AttnArgs a) {
   // derived from it live in scalar registers
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int total = a.meta.n_items[1] * a.n_kv_heads;  // units: work-order slots x kv-heads
+  const int CH = a.meta.n_items[3];                     // keys per item (a multiple of 128)
   const int P = a.kv.page_size;
   // key row of this lane in S^T tile t (within a 32-key block); tile 1 adds 4
   const int kk0 = (ln >> 2) * 8 + (ln & 3);
@@ -110,7 +111,7 @@ k_attn(AttnArgs a) {
     int nrows = nt * a.G;
     if (shared)
       for (int jm = 1; jm < nmem; ++jm) nrows += min(a.TB, a.meta.req_ntok[b + jm]) * a.G;
-    const int last_pos = shared ? (chunk + 1) * a.chunk - 1 : pos0 + t0 + nt - 1;
+    const int last_pos = shared ? (chunk + 1) * CH - 1 : pos0 + t0 + nt - 1;
     const int qpos0 = shared ? last_pos + 1 : pos0 + t0;  // smallest row position
     // tree drafts: every key at or past the context needs its row's node mask
     // (a shared-prefix unit's keys all precede the context)
@@ -130,8 +131,8 @@ k_attn(AttnArgs a) {
       __syncthreads();
     }
     const int S = last_pos + 1;
-    const int kbeg = chunk * a.chunk, kend = min(S, kbeg + a.chunk);
-    const int CW = a.chunk / 4;
+    const int kbeg = chunk * CH, kend = min(S, kbeg + CH);
+    const int CW = CH / 4;
     const int wk0 = kbeg + w * CW, wk1 = min(kend, wk0 + CW);
     const int nb = wk1 > wk0 ? (wk1 - wk0 + 31) / 32 : 0;
     // blocks before nfull lie at or below every row's position (and inside the

@@ -92,7 +92,7 @@ struct StepMeta {
   // nullable: the attention work order, n_items[1] item slots.  An item with
   // .w > 0 is a shared-prefix unit covering the rows of requests x .. x+w-1.
   int32_t* order;
-  int32_t* n_items;     // [0] item slots, [1] units in the work order
+  int32_t* n_items;     // [0] item slots, [1] units in the work order, [3] keys per item
   // the work order resolved: per slot of the order, two int4
   //   (item, request, key chunk, first token | rows' token count << 16),
   //   (.w of the item, sequence id, request position 0, request's first row)

@@ -20,7 +20,9 @@ struct KvGeom {
 };
 
 struct VerifySetupArgs {
-  int B, k_max, vocab, chunk;
+  int B, k_max, vocab;
+  int chunk;         // keys per attention item; doubled when that still leaves
+  int items_double;  // at least this many items (enough to fill the attention grid)
   int G;        // query heads per kv-head
   int rb;       // attention row block of the step (rows per unit)
   int cascade;  // 1: plan shared-prefix attention units for forked siblings
@@ -60,7 +62,7 @@ struct AttnArgs {
   const int32_t* table;
   int max_pages;
   StepMeta meta;
-  int G, TB, chunk, n_kv_heads;
+  int G, TB, n_kv_heads;
   int prb;           // rows per (item, kv-head) in the partials (the step's row block)
   float scale_log2;  // log2(e) / sqrt(head_dim)
   float* pm;         // [item][kvh][RB]

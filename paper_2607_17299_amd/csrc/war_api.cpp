@@ -356,7 +356,7 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
   return WAR_OK;
 }
 
-AttnArgs attn_args(war_model* m, war_kv_pool* p, int TB, int chunk) {
+AttnArgs attn_args(war_model* m, war_kv_pool* p, int TB) {
   AttnArgs a{};
   a.q = m->q.as<bf16_t>();
   a.q_stride = m->md.nq * m->md.hd;
@@ -366,7 +366,6 @@ AttnArgs attn_args(war_model* m, war_kv_pool* p, int TB, int chunk) {
   a.meta = m->meta();
   a.G = m->md.nq / m->md.nkv;
   a.TB = TB;
-  a.chunk = chunk;
   a.n_kv_heads = m->md.nkv;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)m->md.hd));
   a.pm = m->pm.as<float>();
@@ -789,6 +788,7 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
   va.k_max = k_max;
   va.vocab = m->md.V;
   va.chunk = chunk;
+  va.items_double = cdiv_i(2 * 512, m->md.nkv);  // 2+ units per workgroup of a full (512) grid
   va.seq_ids = seq_ids;
   va.ctx_lens = ctx_lens;
   va.last_tokens = last_tokens;
@@ -808,7 +808,7 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
     launch_verify_setup(p->dev, va, m->meta(), st);
   }
 
-  AttnArgs a = attn_args(m, p, kp1, chunk);
+  AttnArgs a = attn_args(m, p, kp1);
   a.prb = RB;
   // persistent grid = resident capacity: 2 workgroups per CU
   const int grid = (int)std::min<int64_t>(max_items * m->md.nkv, 512);
@@ -1037,12 +1037,13 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
     HIPCHK(h2d(meta.seg_rb, sg_rb.data(), nseg * 4));
     HIPCHK(h2d(meta.items, items.data(), items.size() * sizeof(int4)));
     HIPCHK(h2d(meta.udesc, udesc.data(), udesc.size() * sizeof(int4)));
-    const int32_t ni2[2] = {(int32_t)items.size(), (int32_t)items.size()};  // prefill: the work order is the item list
-    const int32_t ni = ni2[0];
-    HIPCHK(h2d(meta.n_items, ni2, 8));
+    // prefill: the work order is the item list
+    const int32_t ni4[4] = {(int32_t)items.size(), (int32_t)items.size(), 0, chunk};
+    const int32_t ni = ni4[0];
+    HIPCHK(h2d(meta.n_items, ni4, 16));
     HIPCHK(hipStreamSynchronize(st));  // host vectors go out of scope below
 
-    AttnArgs a = attn_args(m, p, TB, chunk);
+    AttnArgs a = attn_args(m, p, TB);
     a.meta.order = nullptr;  // prefill items run in list order
     a.prb = RB;
     const int grid = (int)std::min<int64_t>((int64_t)ni * m->md.nkv, 512);
