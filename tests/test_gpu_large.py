@@ -319,11 +319,13 @@ def _oracle_kv_stream(cfg, kv_seed, seq, ctx, tag):
     return kv_get
 
 
-def _full_size_check(st, kv_seed, sample, tag, setup=None):
+def _full_size_check(st, kv_seed, sample, tag, setup=None, chunk=None):
     """Run one verify step of the 36-layer model on the GPU with logits and
     recompute the sampled requests with the oracle (float64, and its fp32-
     accumulation mode for the tolerance), layer by layer.  `setup`, when given,
-    builds (model, pool, step, kv_get factory) instead of the seeded contexts."""
+    builds (model, pool, step, kv_get factory) instead of the seeded contexts.
+    `chunk`, when given, is the attention chunk length the step must have used
+    (the step setup picks 1024 or 2048 keys per item)."""
     war = _war()
     cfg = synth.LARGE
     w = harness.large_weights(cfg)
@@ -336,6 +338,10 @@ def _full_size_check(st, kv_seed, sample, tag, setup=None):
         model, pool, st, kv_source = setup(war, cfg, w)
     ds = harness.DeviceStep(st, with_logits=True, vocab=cfg.vocab)
     ds.verify(model, pool, logits=True)
+    torch.cuda.synchronize()
+    if chunk is not None:
+        n_items = war.debug_workspace(model, "n_items", torch.int32, (4,)).cpu().tolist()
+        assert n_items[3] == chunk, (tag, n_items)
     ds.commit(pool, discard=False)
     torch.cuda.synchronize()
     glog = ds.logits.cpu().numpy().reshape(st.B, st.k_max + 1, cfg.vocab)
@@ -361,8 +367,9 @@ def _full_size_check(st, kv_seed, sample, tag, setup=None):
 
 def test_full_size_low_load_sampled():
     """The benchmark's workload at full size (36 layers, 8 x 32768, k = 8);
-    request 0 is recomputed by the oracle."""
-    _full_size_check(harness.low_load_step(), 5, [0], "low_load")
+    request 0 is recomputed by the oracle.  The batch has enough keys for
+    2048-key attention chunks (8 x 17 items), so those are what it checks."""
+    _full_size_check(harness.low_load_step(), 5, [0], "low_load", chunk=2048)
 
 
 def test_full_size_high_load_sampled():
@@ -401,7 +408,8 @@ def test_full_size_multi_turn_sampled():
                 return cache[l]
             return kv_get
         return model, pool, st, kv_source
-    _full_size_check(None, 5, [0, 5], "multi_turn", setup=setup)
+    # forked siblings keep 1024-key chunks (shared chunks read together hit L2)
+    _full_size_check(None, 5, [0, 5], "multi_turn", setup=setup, chunk=1024)
 
 
 def test_full_size_high_load_k2_sampled():
