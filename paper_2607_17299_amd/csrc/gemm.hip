@@ -58,15 +58,21 @@ struct Tile {
 // fully unrolled (straight-line code lets the compiler's memory-counter waits
 // stay exact, so loads issued three steps ahead really stay in flight);
 // NSTEPS == 0: a runtime loop over (K split) / 64 steps.
-template <int MT, int NSTEPS, int EPI>
-__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm(GemmArgs g) {
-  __shared__ __attribute__((aligned(16))) unsigned char sA[3][Tile<MT>::BYTES];
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
+// MW = 2: two groups of 4 waves take the two m-blocks of one weight block in
+// one workgroup (rows 97-192: one workgroup per CU instead of 1.5); both read
+// the same W fragments, the second group mostly from L1/L2.
+template <int MT, int NSTEPS, int EPI, int MW>
+__global__ void __launch_bounds__(256 * MW) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm(GemmArgs g) {
+  static_assert(MW == 1 || EPI != EPI_ARGMAX, "the argmax epilogue has one m-block per workgroup");
+  __shared__ __attribute__((aligned(16))) unsigned char sAll[MW][3][Tile<MT>::BYTES];
+  const int tid = threadIdx.x & 255, lane = tid & 63, w = tid >> 6, ln = lane & 15, lg = lane >> 4;
+  const int mg = MW > 1 ? __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 8) : 0;
+  unsigned char (*sA)[Tile<MT>::BYTES] = sAll[mg];
   // Workgroups are dealt to the 8 XCDs round-robin by linear id.  The m-blocks
   // of one weight block get ids 8 apart (same XCD, dispatched together), so
   // all but the first find W in that XCD's L2; a ragged tail of fewer than 8
   // n-blocks falls back to consecutive ids.
-  const int mblocks = (g.M + MT * 16 - 1) / (MT * 16);
+  const int mblocks = (g.M + MT * 16 * MW - 1) / (MT * 16 * MW);  // workgroup m-blocks
   const int NB = g.N / 128;
   const int full = (NB / 8) * 8 * mblocks;
   int nb, mb;
@@ -80,7 +86,7 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
     mb = r % mblocks;
   }
   const int split = blockIdx.y;
-  const int m0 = mb * MT * 16;
+  const int m0 = (mb * MW + mg) * MT * 16;
   const int kb = split * g.kper;
   const int ke = min(g.K, kb + g.kper);
   const int nsteps = NSTEPS > 0 ? NSTEPS : (ke - kb) / KS;
@@ -273,32 +279,43 @@ __global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 2))
   }
 }
 
-template <int MT>
-void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
-  dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 16), splits, 1);
+template <int MT, int MW>
+void launch_mw(const GemmArgs& g, int epi, int splits, hipStream_t st) {
+  dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 16 * MW), splits, 1);
+  const dim3 block(256 * MW);
   const int steps = g.kper / KS;
   const bool exact = (int64_t)g.kper * splits == g.K;
-  if (epi == EPI_ARGMAX) {
-    k_gemm<MT, 0, EPI_ARGMAX><<<grid, 256, 0, st>>>(g);
-  } else if (epi == EPI_SWIGLU) {
-    if (steps == 64) k_gemm<MT, 64, EPI_SWIGLU><<<grid, 256, 0, st>>>(g);
-    else k_gemm<MT, 0, EPI_SWIGLU><<<grid, 256, 0, st>>>(g);
+  if (epi == EPI_SWIGLU) {
+    if (steps == 64) k_gemm<MT, 64, EPI_SWIGLU, MW><<<grid, block, 0, st>>>(g);
+    else k_gemm<MT, 0, EPI_SWIGLU, MW><<<grid, block, 0, st>>>(g);
   } else if (exact && steps == 4) {
-    k_gemm<MT, 4, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+    k_gemm<MT, 4, EPI_PARTIAL, MW><<<grid, block, 0, st>>>(g);
   } else if (exact && steps == 8) {
-    k_gemm<MT, 8, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+    k_gemm<MT, 8, EPI_PARTIAL, MW><<<grid, block, 0, st>>>(g);
   } else if (exact && steps == 12) {
-    k_gemm<MT, 12, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+    k_gemm<MT, 12, EPI_PARTIAL, MW><<<grid, block, 0, st>>>(g);
   } else if (exact && steps == 16) {
-    k_gemm<MT, 16, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+    k_gemm<MT, 16, EPI_PARTIAL, MW><<<grid, block, 0, st>>>(g);
   } else if (exact && steps == 32) {
-    k_gemm<MT, 32, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+    k_gemm<MT, 32, EPI_PARTIAL, MW><<<grid, block, 0, st>>>(g);
   } else if (exact && steps == 48) {
-    k_gemm<MT, 48, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+    k_gemm<MT, 48, EPI_PARTIAL, MW><<<grid, block, 0, st>>>(g);
   } else if (exact && steps == 64) {
-    k_gemm<MT, 64, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+    k_gemm<MT, 64, EPI_PARTIAL, MW><<<grid, block, 0, st>>>(g);
   } else {
-    k_gemm<MT, 0, EPI_PARTIAL><<<grid, 256, 0, st>>>(g);
+    k_gemm<MT, 0, EPI_PARTIAL, MW><<<grid, block, 0, st>>>(g);
+  }
+}
+
+template <int MT>
+void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
+  if (epi == EPI_ARGMAX) {
+    dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 16), splits, 1);
+    k_gemm<MT, 0, EPI_ARGMAX, 1><<<grid, 256, 0, st>>>(g);
+  } else if (MT <= 6 && gemm_mw(g.M) == 2) {
+    launch_mw<(MT <= 6 ? MT : 6), 2>(g, epi, splits, st);
+  } else {
+    launch_mw<MT, 1>(g, epi, splits, st);
   }
 }
 
@@ -331,12 +348,15 @@ void launch_pack_weights(const bf16_t* W, const bf16_t* W2, int N, int K, bf16_t
   k_pack_weights<<<blocks, 256, 0, st>>>(W, W2, K, chunks, reinterpret_cast<uint4*>(dst), N / 128);
 }
 
-// 16-row tiles per workgroup: up to 6 (96 rows); more rows take more m-blocks
+// 16-row tiles per m-block: up to 6 (96 rows); more rows take more m-blocks
 int gemm_mt(int M) {
   const int t = std::max(1, cdiv_i(M, 16));
   if (t <= 6) return t;
   return cdiv_i(t, cdiv_i(t, 6));  // balanced m-blocks of at most 6 tiles
 }
+
+// m-blocks per workgroup: 2 when the rows make exactly two m-blocks
+int gemm_mw(int M) { return cdiv_i(M, 16 * gemm_mt(M)) == 2 ? 2 : 1; }
 
 void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   switch (gemm_mt(g.M)) {

@@ -243,7 +243,7 @@ struct Timed {
 // (measured on the 4096- and 6144-wide projections: 192-256 is the optimum).
 Split pick_split(int M, int N, int K, int64_t cap_elems) {
   const int mt = gemm_mt(M);
-  const int mblocks = cdiv_i(M, mt * 16);
+  const int mblocks = cdiv_i(M, mt * 16 * gemm_mw(M));  // workgroups per n-block and split
   const int base = (N / 128) * mblocks;
   for (int s = 1; s <= 64; ++s) {
     if (K % (s * 64)) continue;

@@ -84,6 +84,9 @@ def _check_step(env, st, report, tag):
     (2, [2, 0, 1], [700, 3001, 1024]),
     (4, [4, 1, 3], [1500, 33, 2048]),
     (8, [8, 5, 0], [3000, 1100, 2500]),
+    # 108 rows: two 64-row m-blocks, taken by one GEMM workgroup
+    (8, [8, 3, 0, 8, 1, 6, 2, 8, 0, 5, 8, 4],
+     [300, 1200, 77, 2100, 640, 90, 1500, 33, 1025, 400, 260, 700]),
 ])
 def test_reduced_depth_verify_matches_oracle(large2, k, lens, ctxs):
     cfg = large2["cfg"]
