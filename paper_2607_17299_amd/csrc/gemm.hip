@@ -312,8 +312,8 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   if (epi == EPI_ARGMAX) {
     dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 16), splits, 1);
     k_gemm<MT, 0, EPI_ARGMAX, 1><<<grid, 256, 0, st>>>(g);
-  } else if (MT <= 6 && gemm_mw(g.M) == 2) {
-    launch_mw<(MT <= 6 ? MT : 6), 2>(g, epi, splits, st);
+  } else if (gemm_mw(g.M) == 2) {
+    launch_mw<MT, 2>(g, epi, splits, st);
   } else {
     launch_mw<MT, 1>(g, epi, splits, st);
   }
@@ -365,12 +365,6 @@ void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st) {
     case 3: launch_mt<3>(g, epi, splits, st); break;
     case 4: launch_mt<4>(g, epi, splits, st); break;
     case 5: launch_mt<5>(g, epi, splits, st); break;
-    case 6: launch_mt<6>(g, epi, splits, st); break;
-    case 7: launch_mt<7>(g, epi, splits, st); break;
-    case 8: launch_mt<8>(g, epi, splits, st); break;
-    case 9: launch_mt<9>(g, epi, splits, st); break;
-    case 10: launch_mt<10>(g, epi, splits, st); break;
-    case 11: launch_mt<11>(g, epi, splits, st); break;
-    default: launch_mt<12>(g, epi, splits, st); break;
+    default: launch_mt<6>(g, epi, splits, st); break;  // gemm_mt never exceeds 6
   }
 }
