@@ -87,6 +87,7 @@ struct Profiler {
 };
 constexpr int kPrefillChunk = 1024;  // keys per attention item when prefilling
 constexpr int kMaxItemsPerSeq = 512;  // attention chunks one combine merges
+constexpr int kAttnGrid = 512;        // persistent attention grid: 2 workgroups per CU
 constexpr int64_t kPartialCap = int64_t(64) << 20;  // fp32 split-K partial elements
 
 }  // namespace
@@ -788,7 +789,7 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
   va.k_max = k_max;
   va.vocab = m->md.V;
   va.chunk = chunk;
-  va.items_double = cdiv_i(2 * 512, m->md.nkv);  // 2+ units per workgroup of a full (512) grid
+  va.items_double = cdiv_i(2 * kAttnGrid, m->md.nkv);  // 2+ units per workgroup of a full grid
   va.seq_ids = seq_ids;
   va.ctx_lens = ctx_lens;
   va.last_tokens = last_tokens;
@@ -811,7 +812,7 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
   AttnArgs a = attn_args(m, p, kp1);
   a.prb = RB;
   // persistent grid = resident capacity: 2 workgroups per CU
-  const int grid = (int)std::min<int64_t>(max_items * m->md.nkv, 512);
+  const int grid = (int)std::min<int64_t>(max_items * m->md.nkv, kAttnGrid);
   s = run_layers(m, p, R, a, RB, grid, B, st);
   if (s != WAR_OK) return s;
   int sdummy;
@@ -1046,7 +1047,7 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
     AttnArgs a = attn_args(m, p, TB);
     a.meta.order = nullptr;  // prefill items run in list order
     a.prb = RB;
-    const int grid = (int)std::min<int64_t>((int64_t)ni * m->md.nkv, 512);
+    const int grid = (int)std::min<int64_t>((int64_t)ni * m->md.nkv, kAttnGrid);
     s = run_layers(m, p, R, a, RB, std::max(grid, 1), nseg, st);
     if (s != WAR_OK) return s;
     // LM head on the rows that end a sequence inside this chunk
