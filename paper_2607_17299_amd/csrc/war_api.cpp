@@ -998,20 +998,28 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
         pos[rq_row0[j] + t] = rq_pos0[j] + t;
         rreq[rq_row0[j] + t] = j;
       }
-      for (int rb = 0; rb * TB < rq_ntok[j]; ++rb) {
+      // items (and so the merge order) row block by row block; the work order
+      // chunk by chunk, so that the units reading one key chunk for different
+      // row blocks run together and find it in their XCD's L2
+      const int nrb = cdiv_i(rq_ntok[j], TB);
+      const int seg0 = (int)sg_b.size();
+      for (int rb = 0; rb < nrb; ++rb) {
         const int S = rq_pos0[j] + std::min(rq_ntok[j], (rb + 1) * TB);
         const int nch = cdiv_i(S, chunk);
         sg_b.push_back((int32_t)items.size());
         sg_c.push_back(nch);
         sg_r.push_back(j);
         sg_rb.push_back(rb);
-        const int t0 = rb * TB, ntk = std::min(TB, rq_ntok[j] - t0);
-        for (int c = 0; c < nch; ++c) {
-          udesc.push_back(make_int4((int)items.size(), j, c, t0 | (ntk << 16)));
-          udesc.push_back(make_int4(0, rq_seq[j], rq_pos0[j], rq_row0[j]));
-          items.push_back(make_int4(j, rb, c, 0));
-        }
+        for (int c = 0; c < nch; ++c) items.push_back(make_int4(j, rb, c, 0));
       }
+      const int max_nch = sg_c.back();  // the last row block sees the most keys
+      for (int c = 0; c < max_nch; ++c)
+        for (int rb = 0; rb < nrb; ++rb) {
+          if (c >= sg_c[seg0 + rb]) continue;
+          const int t0 = rb * TB, ntk = std::min(TB, rq_ntok[j] - t0);
+          udesc.push_back(make_int4(sg_b[seg0 + rb] + c, j, c, t0 | (ntk << 16)));
+          udesc.push_back(make_int4(0, rq_seq[j], rq_pos0[j], rq_row0[j]));
+        }
     }
     const int nseg = (int)sg_b.size();
     CHECK(nseg <= m->n_seg_cap && nr <= m->n_req_cap, "internal: prefill chunk too fragmented");
