@@ -85,7 +85,7 @@ struct Profiler {
     return pool[used++];
   }
 };
-constexpr int kPrefillChunk = 1024;  // keys per attention item when prefilling
+constexpr int kPrefillChunk = 2048;  // keys per attention item when prefilling (chunk-major: L2 serves the row blocks)
 constexpr int kMaxItemsPerSeq = 512;  // attention chunks one combine merges
 constexpr int kAttnGrid = 512;        // persistent attention grid: 2 workgroups per CU
 constexpr int64_t kPartialCap = int64_t(64) << 20;  // fp32 split-K partial elements
