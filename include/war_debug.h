@@ -25,8 +25,8 @@ war_status war_debug_mfma16(const void* A, const void* B, float* C, void* stream
  * [rows][nq*hd]; "P" fp32 split-K partials; "pm", "pl", "po" attention
  * partials; "rows", "reqs", "items" step metadata; "order" the attention work
  * order and "n_items" its counts ([0] item slots, [1] units in the work
- * order, [3] keys per attention item: 1024 or 2048 in a verify step, as the
- * step setup chose); "tree" the last tree step's node slots and node masks
+ * order, [3] keys per attention item, which a verify step's setup chooses:
+ * the base length or twice it); "tree" the last tree step's node slots and node masks
  * (int32 [2][max_rows]).  The pointer stays valid until the next call on the
  * model. */
 war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes);
