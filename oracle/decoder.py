@@ -122,15 +122,25 @@ KVGetter = Callable[[int], Tuple[np.ndarray, np.ndarray]]
 
 
 def forward_block(cfg, W: Weights, tokens: Sequence[int], pos0: int, kv_get: KVGetter,
-                  rounding: bool = True, want_logits: bool = True, precision: str = "fp64"):
+                  rounding: bool = True, want_logits: bool = True, precision: str = "fp64",
+                  trace: Optional[Dict[str, np.ndarray]] = None):
     """Run tokens (at positions pos0, pos0+1, ...) through the decoder.
 
     ``kv_get(l)`` returns the cached keys and values of layer l for positions
     0..pos0-1 as [Hkv, pos0, D] arrays.  Returns (logits [n, V] or the final
     normalised hidden state when want_logits is False, new_kv) where new_kv[l]
     = (K_new [Hkv, n, D], V_new [Hkv, n, D]) for the block's own tokens.
+
+    ``trace``, when given, receives every intermediate under a name (layer l's
+    as "l{l}.<name>"): h0 (embedding rows), u1 (attention norm output), qkv
+    (projection), q, k, v (after RoPE and rounding), o (attention output),
+    h1 (residual after attention), u2 (FFN norm output), gate, up, y (SwiGLU
+    product), h2 (residual after the FFN), then hf (final norm output) and
+    logits.  Recording copies values only; it changes no arithmetic.
     """
     rb = round_bf16 if rounding else (lambda a: a)
+    rec = (lambda name, a: trace.__setitem__(name, np.array(a, copy=True))) if trace is not None \
+        else (lambda name, a: None)
     if precision == "fp64":
         mm = lambda x, Wt: x @ Wt.T
         attn = attention
@@ -144,30 +154,47 @@ def forward_block(cfg, W: Weights, tokens: Sequence[int], pos0: int, kv_get: KVG
     Hq, Hkv, D = cfg.n_q_heads, cfg.n_kv_heads, cfg.head_dim
     pos = pos0 + np.arange(n)
     h = W.embed_rows(tokens)                                             # [n, d]
+    rec("h0", h)
     new_kv: List[Tuple[np.ndarray, np.ndarray]] = []
     for l in range(cfg.n_layers):
         p = f"l{l}."
         u = rb(rms_norm(h, W.get(p + "attn_norm"), cfg.rms_eps))
+        rec(p + "u1", u)
         qkv = mm(u, W.get(p + "w_qkv"))                                 # [n, qkv]
+        rec(p + "qkv", qkv)
         q = qkv[:, : Hq * D].reshape(n, Hq, D)
         k = qkv[:, Hq * D: (Hq + Hkv) * D].reshape(n, Hkv, D)
         v = qkv[:, (Hq + Hkv) * D:].reshape(n, Hkv, D)
         q = rb(rope(q, pos, cfg.rope_base))
         k = rb(rope(k, pos, cfg.rope_base))
         v = rb(v)
+        rec(p + "q", q)
+        rec(p + "k", k)
+        rec(p + "v", v)
         Kc, Vc = kv_get(l)
         K = np.concatenate([Kc, k.transpose(1, 0, 2)], axis=1)          # [Hkv, pos0+n, D]
         V = np.concatenate([Vc, v.transpose(1, 0, 2)], axis=1)
         new_kv.append((k.transpose(1, 0, 2).copy(), v.transpose(1, 0, 2).copy()))
         o = rb(attn(q, K, V, pos, Hq // Hkv)).reshape(n, Hq * D)
+        rec(p + "o", o)
         h = h + mm(o, W.get(p + "w_o"))
+        rec(p + "h1", h)
         u = rb(rms_norm(h, W.get(p + "ffn_norm"), cfg.rms_eps))
-        y = rb(silu(mm(u, W.get(p + "w_gate"))) * mm(u, W.get(p + "w_up")))
+        rec(p + "u2", u)
+        gate, up = mm(u, W.get(p + "w_gate")), mm(u, W.get(p + "w_up"))
+        rec(p + "gate", gate)
+        rec(p + "up", up)
+        y = rb(silu(gate) * up)
+        rec(p + "y", y)
         h = h + mm(y, W.get(p + "w_down"))
+        rec(p + "h2", h)
     hf = rb(rms_norm(h, W.get("final_norm"), cfg.rms_eps))
+    rec("hf", hf)
     if not want_logits:
         return hf, new_kv
-    return mm(hf, W.get("w_lm")), new_kv
+    z = mm(hf, W.get("w_lm"))
+    rec("logits", z)
+    return z, new_kv
 
 
 class RequestKV:
