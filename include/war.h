@@ -50,7 +50,7 @@ typedef int32_t war_status;
 #define WAR_ERR_OUT_OF_PAGES (-2)
 #define WAR_ERR_HIP          (-3)
 #define WAR_ERR_UNSUPPORTED  (-4)
-#define WAR_ERR_DEVICE       (-5) /* the device flagged bad input (war_pool_check) */
+#define WAR_ERR_DEVICE       (-5) /* the device flagged bad input (war_pool_state) */
 
 /* Decoder shape.
  * Layers: RMSNorm -> QKV -> rotate-half RoPE -> grouped-query attention -> O-proj,
@@ -114,7 +114,12 @@ war_status war_kv_pool_create(const war_model_config* cfg, void* kv_pages, int32
                               void* stream, war_kv_pool** out);
 void war_kv_pool_destroy(war_kv_pool* p);
 
-/* Ensure capacity for n_tokens[i] slots for sequence seq_ids[i] (host arrays, distinct ids). */
+/* Ensure capacity for n_tokens[i] slots for sequence seq_ids[i] (host arrays,
+ * distinct ids).  A trajectory's KV cache grows with its length and stays
+ * resident from turn to turn, so KV memory is the pressure point of rollout
+ * (Background, "Rollout Bottlenecks"; System Design, "Overview of WAR").
+ * Pages are popped from the free stack; nothing changes when they do not
+ * suffice (WAR_ERR_OUT_OF_PAGES).  Synchronises the stream. */
 war_status war_kv_alloc(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host,
                         const int32_t* n_tokens_host, void* stream);
 
@@ -126,13 +131,20 @@ war_status war_kv_fork(war_kv_pool* p, int32_t src_seq, int32_t dst_seq, int32_t
                        void* stream);
 
 /* Drop every page of each listed sequence (host array, distinct ids); a page
- * returns to the free stack when its reference count reaches 0. */
+ * returns to the free stack when its reference count reaches 0.  A finished
+ * trajectory releases the KV memory it held (Background, "Rollout
+ * Bottlenecks": KV footprint limits how many requests a replica keeps).
+ * Synchronises the stream. */
 war_status war_kv_free(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host, void* stream);
 
 /* Write precomputed keys/values of tokens [pos0, pos0 + n) of one layer of one
  * sequence into its pages (capacity must already be there, e.g. war_kv_alloc).
  * src: bf16 [2][n_kv_heads][n][head_dim] (0 = keys after RoPE, 1 = values).
- * Imports a cached context computed elsewhere, such as another replica's. */
+ * Imports a cached context computed elsewhere: the scheduler places a
+ * request on the replica whose cache already holds its prefix, and a
+ * trajectory's KV is reused across turns instead of recomputed (System
+ * Design, "Overview of WAR" and the cache-aware scheduler).  Reads the
+ * sequence's page count (one stream synchronisation). */
 war_status war_kv_load(war_kv_pool* p, int32_t seq_id, int32_t layer, int32_t pos0, int32_t n,
                        const void* src, void* stream);
 
@@ -153,7 +165,7 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
                               float* last_logits, void* stream);
 
 /* One speculative-verification step over B requests (k_max = 0: plain decode).
- *   seq_ids      device int32 [B], distinct
+ *   seq_ids      device int32 [B], distinct (checked on the device)
  *   ctx_lens     device int32 [B]  cached tokens per request (not changed here)
  *   last_tokens  device int32 [B]  pending token (previous step's next_tokens)
  *   draft_tokens device int32 [B][k_max] (may be NULL when k_max == 0)
@@ -164,7 +176,17 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
  *                holds request b's row i; rows with i > draft_len are unspecified.
  * Reserves the pages for ctx + draft_len + 1 slots, writes the KV of all rows,
  * and leaves the pool waiting for war_kv_commit.  Until that commit the pool
- * accepts no other call that changes pages. */
+ * accepts no other call that changes pages.
+ * The device checks what the host cannot see without waiting: ids in range
+ * and distinct, ctx_len >= 0, ctx + draft_len + 1 within max_pages_per_seq,
+ * token ids in [0, vocab), enough free pages.  On a bad id, length or page
+ * count the whole step fails on the device: no page moves, accept_lens and
+ * next_tokens are -1 for every request, the following war_kv_commit changes
+ * nothing, and war_pool_state returns WAR_ERR_DEVICE (a bad token id is
+ * flagged the same way but the step runs with token 0 in its place).  The
+ * host never waits for the device here while its lower bound on the free
+ * pages (kept from each commit's report) covers B * ceil((k_max+1)/16)
+ * pages; otherwise it reads the exact count once. */
 war_status war_verify_step(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
                            const int32_t* ctx_lens, const int32_t* last_tokens,
                            const int32_t* draft_tokens, const int32_t* draft_lens, int32_t k_max,
@@ -227,7 +249,11 @@ war_status war_verify_step_tree(war_model* m, war_kv_pool* p, int32_t B, const i
  *   ctx_lens[b] += accept_lens[b] + 1;
  *   the pages the step reserved beyond the new length go back to the free
  *   stack, and their block-table entries become -1.
- * Use the same B, seq_ids and ctx_lens as the verify step. */
+ * After a step that failed on the device nothing changes.  Use the same B,
+ * seq_ids and ctx_lens as the verify step (an id out of range is flagged and
+ * skipped).  When the kernel ends it writes its sequence number and the free
+ * page count to a host-mapped word of the pool, which later verify steps read
+ * instead of waiting. */
 war_status war_kv_commit(war_kv_pool* p, int32_t B, const int32_t* seq_ids, int32_t* ctx_lens,
                          const int32_t* accept_lens, void* stream);
 
@@ -237,9 +263,10 @@ war_status war_kv_commit(war_kv_pool* p, int32_t B, const int32_t* seq_ids, int3
  *   refcount        [num_pages]
  *   held            [max_seqs]   pages held per sequence
  *   step_base       [max_seqs]   pages held before the last reservation
- * Returns WAR_ERR_DEVICE if a kernel flagged bad device-side input (a token
- * id outside [0, vocab), a tree parent out of range, or a device page
- * shortage). */
+ * Returns WAR_ERR_DEVICE if a kernel flagged bad device-side input since the
+ * last call (a token id outside [0, vocab), a sequence id out of range or
+ * repeated within one step, a negative or too long context, a tree parent out
+ * of range, or a device page shortage); the flags are then cleared. */
 war_status war_pool_state(war_kv_pool* p, int32_t* free_count, int32_t* free_stack,
                           int32_t* refcount, int32_t* held, int32_t* step_base, void* stream);
 

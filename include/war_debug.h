@@ -40,6 +40,11 @@ war_status war_debug_sample(const float* logits, int32_t V, int32_t B, int32_t k
                             const int32_t* drafts, const float* uniforms, float temperature, int32_t top_k,
                             int32_t* accept_lens, int32_t* next_tokens, void* stream);
 
+/* How many times the pool's verify steps read the exact free page count from
+ * the device (each such read waits for the stream) because the host's lower
+ * bound did not cover the step's worst-case reservation (HOST out). */
+war_status war_debug_pool_waits(war_kv_pool* p, int64_t* waits);
+
 /* Per-kernel timing.  war_profile(m, 1) clears the record and starts timing
  * every kernel launch of later verify/prefill calls on this model.  Each
  * launch is bracketed by a pair of HIP events on the launch stream.

@@ -52,6 +52,7 @@ __global__ void k_pool_init(PoolDev p) {
     if (i == 0) {
       p.scalars[0] = p.num_pages;
       p.scalars[1] = 0;
+      p.scalars[2] = 0;
     }
   }
 }
@@ -109,10 +110,18 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
   __shared__ int s_ctx[kBT], s_dl[kBT];
   __shared__ int s_pg0[kBT], s_nch[kBT], s_seq[kBT], s_shr[kBT], s_noff[kBT], s_run[kBT];
   __shared__ int s_lead[kBT], s_np[kBT], s_mis[kBT];
+  constexpr int kHash = 2 * kBT;  // open-addressing table of the step's ids
+  __shared__ int s_hash[kHash];
   const int t = threadIdx.x;
   const int kp1 = a.k_max + 1;
-  __shared__ int s_bad;
-  if (t == 0) s_bad = 0;
+  __shared__ int s_bad, s_dup;
+  if (t == 0) {
+    s_bad = 0;
+    s_dup = 0;
+  }
+  // the attention launches of this step start their work counters at zero
+  if (t < 8) a.unit_ctr[t] = 0;
+  for (int i = t; i < kHash; i += kBT) s_hash[i] = -1;
   __syncthreads();
   int s = 0, need = 0, ctx = 0, dl = 0, hb = 0;
   if (t < a.B) {
@@ -128,16 +137,29 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
       ctx = 0;
       atomicOr(&s_bad, 1);
     } else {
+      // two entries with one id would pop into the same block-table row:
+      // insert the id (linear probing; B <= kBT ids never fill the table)
+      unsigned hsh = ((unsigned)s * 2654435761u) >> 21;
+      for (int probe = 0; probe < kHash; ++probe) {
+        const int prev = atomicCAS(&s_hash[hsh], -1, s);
+        if (prev == -1) break;
+        if (prev == s) {
+          atomicOr(&s_dup, 1);
+          break;
+        }
+        hsh = (hsh + 1) & (kHash - 1);
+      }
       hb = p.held[s];
       need = max(0, cdiv_i(ctx + dl + 1, p.page_size) - hb);
     }
   }
   int total;
-  const int off = block_excl_scan(need, sh, &total);
+  const int off = block_excl_scan(need, sh, &total);  // (its barriers order the inserts)
   const int fc = p.scalars[0];
   if (t == 0) {
-    s_fail = total > fc || s_bad;
+    s_fail = total > fc || s_bad || s_dup;
     if (s_bad) atomicOr(&p.scalars[1], ERR_BAD_TOKEN);
+    if (s_dup) atomicOr(&p.scalars[1], ERR_DUP_SEQ);
   }
   __syncthreads();
   const bool fail = s_fail;
@@ -265,8 +287,9 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
     m.n_items[1] = n_units;
     m.n_items[2] = 0;
     m.n_items[3] = chunk;
-    if (fail && !s_bad) p.scalars[1] |= ERR_NO_PAGES;
+    if (fail && !s_bad && !s_dup) p.scalars[1] |= ERR_NO_PAGES;
     if (!fail) p.scalars[0] = fc - total;
+    p.scalars[2] = fail ? 1 : 0;  // the commit of a failed step changes nothing
   }
   __syncthreads();
   // rows: request b's token i sits in row b*(k_max+1)+i
@@ -311,15 +334,36 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
 }
 
 // Commit: keep ctx + a + 1 tokens, push the step's pages beyond them
-// (entries in descending order, logical pages descending).
+// (entries in descending order, logical pages descending).  After a verify
+// step whose setup failed nothing changes.  Thread 0 then reports
+// (commit_seq, free count) to the host-mapped word.
 __global__ void __launch_bounds__(kBT) k_commit(PoolDev p, int B, const int32_t* seq_ids,
-                                                int32_t* ctx_lens, const int32_t* accept) {
+                                                int32_t* ctx_lens, const int32_t* accept,
+                                                uint32_t commit_seq) {
   __shared__ int sh[16];
+  __shared__ int s_skip;
   const int t = threadIdx.x;
+  if (t == 0) s_skip = p.scalars[2];
+  __syncthreads();
+  if (s_skip) {
+    if (t == 0) {
+      p.scalars[2] = 0;
+      __hip_atomic_store(p.report, ((unsigned long long)commit_seq << 32) | (uint32_t)p.scalars[0],
+                         __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
+    return;
+  }
   const int rt = B - 1 - t;  // entry handled by this thread, so the scan runs descending
   int s = 0, h = 0, keep = 0, rel = 0, new_ctx = 0;
+  bool ok = false;
   if (t < B) {
     s = seq_ids[rt];
+    // the verify step accepted these ids; other ids (a different array than
+    // the step's) are flagged and left alone
+    ok = s >= 0 && s < p.max_seqs;
+    if (!ok) atomicOr(&p.scalars[1], ERR_BAD_TOKEN);
+  }
+  if (ok) {
     h = p.held[s];
     const int ctx = ctx_lens[rt];
     const int cap = h * p.page_size;
@@ -331,7 +375,7 @@ __global__ void __launch_bounds__(kBT) k_commit(PoolDev p, int B, const int32_t*
   int total;
   const int off = block_excl_scan(rel, sh, &total);
   const int fc = p.scalars[0];
-  if (t < B) {
+  if (ok) {
     int32_t* row = p.table + (int64_t)s * p.max_pages;
     for (int j = 0; j < rel; ++j) {
       const int page = row[h - 1 - j];
@@ -344,7 +388,11 @@ __global__ void __launch_bounds__(kBT) k_commit(PoolDev p, int B, const int32_t*
     ctx_lens[rt] = new_ctx;
   }
   __syncthreads();
-  if (t == 0) p.scalars[0] = fc + total;
+  if (t == 0) {
+    p.scalars[0] = fc + total;
+    __hip_atomic_store(p.report, ((unsigned long long)commit_seq << 32) | (uint32_t)(fc + total),
+                       __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+  }
 }
 
 // Free sequences: entries in descending order; within one, logical pages
@@ -441,8 +489,8 @@ void launch_verify_setup(const PoolDev& p, const VerifySetupArgs& a, const StepM
   k_verify_setup<<<1, kBT, 0, st>>>(p, a, m);
 }
 void launch_commit(const PoolDev& p, int B, const int32_t* seq, int32_t* ctx, const int32_t* acc,
-                   hipStream_t st) {
-  k_commit<<<1, kBT, 0, st>>>(p, B, seq, ctx, acc);
+                   uint32_t commit_seq, hipStream_t st) {
+  k_commit<<<1, kBT, 0, st>>>(p, B, seq, ctx, acc, commit_seq);
 }
 void launch_free(const PoolDev& p, int n, const int32_t* seq, hipStream_t st) {
   k_free<<<1, kBT, 0, st>>>(p, n, seq);

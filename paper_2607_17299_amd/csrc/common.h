@@ -68,8 +68,12 @@ struct PoolDev {
   int32_t* refcount;   // [num_pages]
   int32_t* held;       // [max_seqs] pages held per sequence
   int32_t* base;       // [max_seqs] pages held before the last reservation
-  int32_t* scalars;    // [0] free_count, [1] error flags
+  int32_t* scalars;    // [0] free_count, [1] error flags, [2] 1 while a failed
+                       // verify step waits for its commit
   int32_t* table;      // [max_seqs][max_pages] (caller memory)
+  // host-mapped word the commit kernel writes when it ends: (commit sequence
+  // number << 32) | free count, read by the host without waiting
+  unsigned long long* report;
   int32_t num_pages, max_seqs, max_pages, page_size;
 };
 
@@ -108,4 +112,4 @@ struct StepMeta {
   uint32_t* tmask;
 };
 
-enum { ERR_BAD_TOKEN = 1, ERR_NO_PAGES = 2, ERR_BAD_PARENT = 4 };
+enum { ERR_BAD_TOKEN = 1, ERR_NO_PAGES = 2, ERR_BAD_PARENT = 4, ERR_DUP_SEQ = 8 };

@@ -21,6 +21,7 @@ struct KvGeom {
 
 struct VerifySetupArgs {
   int B, k_max, vocab;
+  int32_t* unit_ctr;  // attention work counters [8], cleared here
   int chunk;         // keys per attention item; doubled when that still leaves
   int items_double;  // at least this many items (enough to fill the attention grid)
   int G;        // query heads per kv-head
@@ -80,7 +81,7 @@ void launch_grow(const PoolDev& p, int n, const int32_t* seq, const int32_t* a, 
 void launch_verify_setup(const PoolDev& p, const VerifySetupArgs& a, const StepMeta& m,
                          hipStream_t st);
 void launch_commit(const PoolDev& p, int B, const int32_t* seq, int32_t* ctx, const int32_t* acc,
-                   hipStream_t st);
+                   uint32_t commit_seq, hipStream_t st);
 void launch_free(const PoolDev& p, int n, const int32_t* seq, hipStream_t st);
 void launch_fork(const PoolDev& p, int src, int dst, int npg, hipStream_t st);
 void launch_kv_load(const PoolDev& p, const KvGeom& g, int seq, int layer, int pos0, int n,

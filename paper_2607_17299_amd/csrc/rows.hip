@@ -244,7 +244,9 @@ __global__ void __launch_bounds__(256) k_argmax_accept(const int32_t* ntok, int 
   } else if (parents) {
     for (int d = 0; d < k_max; ++d) accept_path[(int64_t)b * k_max + d] = -1;
   }
-  if (accept_lens) accept_lens[b] = a;
+  // no rows: the step's setup failed (war_pool_state reports why); -1 makes the
+  // commit a discard
+  if (accept_lens) accept_lens[b] = n > 0 ? a : -1;
   next_tokens[b] = n > 0 ? greedy[last] : -1;
 }
 

@@ -253,8 +253,8 @@ __global__ void k_sample_accept(SampleArgs s, int32_t* accept_lens, int32_t* nex
   const int b = blockIdx.x * blockDim.x + threadIdx.x;
   if (b >= s.B) return;
   const int dl = s.ntok[b] - 1;
-  if (dl < 0) {
-    if (accept_lens) accept_lens[b] = 0;
+  if (dl < 0) {  // no rows: the step's setup failed
+    if (accept_lens) accept_lens[b] = -1;
     next_tokens[b] = -1;
     return;
   }

@@ -90,6 +90,106 @@ constexpr int kMaxItemsPerSeq = 512;  // attention chunks one combine merges
 constexpr int kAttnGrid = 512;        // persistent attention grid: 2 workgroups per CU
 constexpr int64_t kPartialCap = int64_t(64) << 20;  // fp32 split-K partial elements
 
+// Everything a forward pass's kernels use besides the caller's arrays and the
+// model's weights, as views of ONE device allocation: activations, split-K
+// partials, RoPE table, LM-head argmax partials, step metadata and the
+// attention work list and partials.  The model owns one such allocation
+// (grown on demand); a verify step may lay the same views over a fixed
+// region instead.
+struct Workspace {
+  float* h;          // residual [R][d] fp32
+  bf16_t* u;         // norm output [R][d]
+  bf16_t* q;         // rotated queries [R][nq*hd]
+  bf16_t* o;         // attention output [R][nq*hd]
+  bf16_t* y;         // SwiGLU output [R][F]
+  float* P;          // split-K partials [p_elems]
+  float *cos_t, *sin_t;          // [R][hd/2]
+  float* amax_v;                 // [R][V/128]
+  int32_t* amax_i;               // [R][V/128]
+  int32_t* rows;                 // tok, pos, active, row_req [4][R]
+  int32_t* tree;                 // kvpos, tmask [2][R]
+  int32_t* reqs;                 // seq, pos0, ntok, row0 [4][n_req_cap]
+  int32_t* segs;                 // begin, count, req, rb [4][n_seg_cap]
+  int32_t* n_items;              // [4]
+  int32_t* unit_ctr;             // [8], zero between attention launches
+  int32_t* a_rows;               // [kMaxBatch] LM-head rows of a prefill chunk
+  int4* items;                   // [items_cap]
+  int4* udesc;                   // [2 * items_cap]
+  int32_t* order;                // [items_cap]
+  float *pm, *pl, *po;           // [items_cap][nkv][rb_cap] (po: x hd)
+  int R = 0, n_req_cap = 0, n_seg_cap = 0, rb_cap = 0;
+  int64_t items_cap = 0, p_elems = 0;
+  bool tree_step = false;        // the metadata describes tree drafts
+
+  StepMeta meta() const {
+    StepMeta m;
+    m.tok = rows;
+    m.pos = rows + R;
+    m.active = rows + 2 * R;
+    m.row_req = rows + 3 * R;
+    m.req_seq = reqs;
+    m.req_pos0 = reqs + n_req_cap;
+    m.req_ntok = reqs + 2 * n_req_cap;
+    m.req_row0 = reqs + 3 * n_req_cap;
+    m.items = items;
+    m.udesc = udesc;
+    m.order = order;
+    m.n_items = n_items;
+    m.seg_begin = segs;
+    m.seg_count = segs + n_seg_cap;
+    m.seg_req = segs + 2 * n_seg_cap;
+    m.seg_rb = segs + 3 * n_seg_cap;
+    m.kvpos = tree_step ? tree : nullptr;
+    m.tmask = tree_step ? reinterpret_cast<uint32_t*>(tree + R) : nullptr;
+    return m;
+  }
+};
+
+// Lays a workspace out from `base` (nullptr: measure only); returns its bytes.
+size_t ws_layout(const ModelDims& md, int R, int64_t items, int rb, int64_t p_elems, char* base,
+                 Workspace* w) {
+  size_t off = 0;
+  auto take = [&](size_t bytes) -> char* {
+    char* at = base ? base + off : nullptr;
+    off += (bytes + 255) & ~size_t(255);
+    return at;
+  };
+  Workspace v;
+  v.R = R;
+  v.n_req_cap = std::max(R, kMaxBatch);
+  v.n_seg_cap = R + kMaxBatch;
+  v.items_cap = std::max<int64_t>(items, 1);
+  v.rb_cap = rb;
+  v.p_elems = p_elems;
+  const size_t nqhd = (size_t)md.nq * md.hd, nb = (size_t)md.V / 128;
+  v.h = reinterpret_cast<float*>(take((size_t)R * md.d * 4));
+  v.u = reinterpret_cast<bf16_t*>(take((size_t)R * md.d * 2));
+  v.q = reinterpret_cast<bf16_t*>(take((size_t)R * nqhd * 2));
+  v.o = reinterpret_cast<bf16_t*>(take((size_t)R * nqhd * 2));
+  v.y = reinterpret_cast<bf16_t*>(take((size_t)R * md.F * 2));
+  v.P = reinterpret_cast<float*>(take((size_t)p_elems * 4));
+  v.cos_t = reinterpret_cast<float*>(take((size_t)R * md.hd / 2 * 4));
+  v.sin_t = reinterpret_cast<float*>(take((size_t)R * md.hd / 2 * 4));
+  v.amax_v = reinterpret_cast<float*>(take((size_t)R * nb * 4));
+  v.amax_i = reinterpret_cast<int32_t*>(take((size_t)R * nb * 4));
+  v.rows = reinterpret_cast<int32_t*>(take((size_t)4 * R * 4));
+  v.tree = reinterpret_cast<int32_t*>(take((size_t)2 * R * 4));
+  v.reqs = reinterpret_cast<int32_t*>(take((size_t)4 * v.n_req_cap * 4));
+  v.segs = reinterpret_cast<int32_t*>(take((size_t)4 * v.n_seg_cap * 4));
+  v.n_items = reinterpret_cast<int32_t*>(take(16));
+  v.unit_ctr = reinterpret_cast<int32_t*>(take(8 * 4));
+  v.a_rows = reinterpret_cast<int32_t*>(take((size_t)kMaxBatch * 4));
+  v.items = reinterpret_cast<int4*>(take((size_t)v.items_cap * sizeof(int4)));
+  v.udesc = reinterpret_cast<int4*>(take((size_t)v.items_cap * 2 * sizeof(int4)));
+  v.order = reinterpret_cast<int32_t*>(take((size_t)v.items_cap * 4));
+  const size_t pr = (size_t)v.items_cap * md.nkv * rb;
+  v.pm = reinterpret_cast<float*>(take(pr * 4));
+  v.pl = reinterpret_cast<float*>(take(pr * 4));
+  v.po = reinterpret_cast<float*>(take(pr * md.hd * 4));
+  if (w) *w = v;
+  return off;
+}
+
 }  // namespace
 
 struct war_model {
@@ -101,51 +201,28 @@ struct war_model {
   const bf16_t* w_lm;
   DevBuf wts;  // owned copy of every weight (matrices packed)
   int max_rows;
-  // workspace
-  DevBuf h, u, q, o, y, P, cos_t, sin_t, inv_freq, amax_v, amax_i;
-  DevBuf rows_i32;  // tok, pos, active, row_req  [4][max_rows]
-  DevBuf reqs_i32;  // seq, pos0, ntok, row0      [4][n_req_cap]
-  DevBuf segs_i32;  // begin, count, req, rb      [4][n_seg_cap]
-  DevBuf n_items, items, order, udesc, pm, pl, po, a_rows;
-  DevBuf unit_ctr;  // attention work counters [8], zero between launches
+  DevBuf inv_freq;  // RoPE frequencies [hd/2] fp64
+  DevBuf ws_buf;    // the model's own workspace allocation
+  Workspace ws;     // views into ws_buf
   DevBuf logits_ws, row_out;  // sampled verification: full logits, per-row outcomes
-  DevBuf tree_i32;            // tree drafts: kvpos, tmask [2][max_rows]
   DevBuf path_ws;             // tree drafts: accepted path when the caller passes none
-  bool tree_step = false;     // the metadata describes tree drafts
-  int n_req_cap, n_seg_cap;
   std::vector<int32_t> h_stage;  // host staging for prefill metadata
   DevBuf stage_dev;              // device copy of per-prefill host arrays
   int32_t* pinned = nullptr;     // pinned host staging
   size_t pinned_ints = 0;
   Profiler prof;
-
-  StepMeta meta() const {
-    StepMeta m;
-    int32_t* r = rows_i32.as<int32_t>();
-    m.tok = r;
-    m.pos = r + max_rows;
-    m.active = r + 2 * max_rows;
-    m.row_req = r + 3 * max_rows;
-    int32_t* q4 = reqs_i32.as<int32_t>();
-    m.req_seq = q4;
-    m.req_pos0 = q4 + n_req_cap;
-    m.req_ntok = q4 + 2 * n_req_cap;
-    m.req_row0 = q4 + 3 * n_req_cap;
-    m.items = items.as<int4>();
-    m.udesc = udesc.as<int4>();
-    m.order = order.as<int32_t>();
-    m.n_items = n_items.as<int32_t>();
-    int32_t* s4 = segs_i32.as<int32_t>();
-    m.seg_begin = s4;
-    m.seg_count = s4 + n_seg_cap;
-    m.seg_req = s4 + 2 * n_seg_cap;
-    m.seg_rb = s4 + 3 * n_seg_cap;
-    int32_t* t2 = tree_i32.as<int32_t>();
-    m.kvpos = tree_step ? t2 : nullptr;
-    m.tmask = tree_step ? reinterpret_cast<uint32_t*>(t2 + max_rows) : nullptr;
-    return m;
-  }
 };
+
+// Host view of the pool's free pages.  A verify step needs a lower bound of
+// the device's free count without waiting for the device:
+//  - an exact count is known after every call that synchronises (base_fc,
+//    with total_need and commit_issued at that time);
+//  - every verify step adds the most pages it can take to total_need;
+//  - every commit kernel, when it ends, writes (its sequence number, the free
+//    count) to a host-mapped word; need_at[j % kRing] is total_need when
+//    commit j was issued, so fc_j - (total_need - need_at[j]) bounds the count
+//    after every step issued since.
+constexpr int kRing = 1024;
 
 struct war_kv_pool {
   war_model_config cfg;
@@ -155,7 +232,12 @@ struct war_kv_pool {
   DevBuf tmp;      // device copies of host id arrays
   int32_t* pinned = nullptr;
   size_t pinned_ints = 0;
-  int64_t free_lb;  // host lower bound of the device free count
+  unsigned long long* report = nullptr;  // host-mapped (commit sequence << 32) | free count
+  int64_t base_fc = 0, base_total = 0;
+  uint32_t base_seq = 0, commit_issued = 0;
+  int64_t total_need = 0;
+  int64_t need_at[kRing] = {};
+  int64_t exact_waits = 0;  // verify steps that read the exact count
   bool pending = false;
   int pending_B = 0;
   bool forked = false;  // some sequences may share pages (war_kv_fork was called)
@@ -257,8 +339,19 @@ Split pick_split(int M, int N, int K, int64_t cap_elems) {
   return {cdiv_i(K, kper), kper};
 }
 
+// Split-K partial elements the projections of an R-row pass write at most.
+int64_t partials_needed(const ModelDims& md, int R) {
+  int64_t n = 1;
+  const int shapes[3][2] = {{md.qkv, md.d}, {md.d, md.nq * md.hd}, {md.d, md.F}};
+  for (const auto& nk : shapes) {
+    const Split sp = pick_split(R, nk[0], nk[1], kPartialCap);
+    n = std::max<int64_t>(n, (int64_t)sp.s * R * nk[0]);
+  }
+  return n;
+}
+
 // One projection: P[split][M][N] = A x W^T (or the LM-head argmax epilogue).
-war_status gemm(war_model* m, const bf16_t* A, int lda, const int32_t* a_rows, const bf16_t* Wp,
+war_status gemm(const Workspace& w, const bf16_t* A, int lda, const int32_t* a_rows, const bf16_t* Wp,
                 int M, int N, int K, int* splits_out, hipStream_t st, bool argmax = false,
                 float* logits = nullptr, bf16_t* swiglu_out = nullptr) {
   GemmArgs g{};
@@ -271,54 +364,56 @@ war_status gemm(war_model* m, const bf16_t* A, int lda, const int32_t* a_rows, c
   g.K = K;
   // the paired gate/up layout is only read by the SwiGLU epilogue: one split
   Split sp{1, K};
-  if (!argmax && !swiglu_out) sp = pick_split(M, N, K, (int64_t)(m->P.bytes / 4));
+  if (!argmax && !swiglu_out) {
+    sp = pick_split(M, N, K, kPartialCap);
+    if ((int64_t)sp.s * M * N > w.p_elems) return fail(WAR_ERR_INVALID_ARG, "internal: split-K partials exceed the workspace");
+  }
   g.kper = sp.kper;
   const bool fuse = swiglu_out != nullptr;
   g.out = swiglu_out;
   g.ld_out = N / 2;
-  g.P = m->P.as<float>();
+  g.P = w.P;
   g.logits = logits;
   g.ld_logits = N;
-  g.amax_v = m->amax_v.as<float>();
-  g.amax_i = m->amax_i.as<int32_t>();
+  g.amax_v = w.amax_v;
+  g.amax_i = w.amax_i;
   launch_gemm(g, argmax ? EPI_ARGMAX : fuse ? EPI_SWIGLU : EPI_PARTIAL, sp.s, st);
   if (splits_out) *splits_out = sp.s;
   return WAR_OK;
 }
 
-// The decoder body over `R` rows whose metadata is in m->meta(); the final
-// normalised hidden state ends in m->u.
-war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_base, int RB,
-                      int attn_grid, int n_segs, hipStream_t st) {
+#define WARCHK(x)                      \
+  do {                                 \
+    war_status s_ = (x);               \
+    if (s_ != WAR_OK) return s_;       \
+  } while (0)
+
+// The decoder body over `R` rows whose metadata is in w.meta(); the final
+// normalised hidden state ends in w.u.
+war_status run_layers(war_model* m, const Workspace& w, war_kv_pool* p, int R, const AttnArgs& attn_base,
+                      int RB, int attn_grid, int n_segs, hipStream_t st) {
   const ModelDims& md = m->md;
-  const StepMeta meta = m->meta();
-  float* h = m->h.as<float>();
-  bf16_t* u = m->u.as<bf16_t>();
-  bf16_t* q = m->q.as<bf16_t>();
-  bf16_t* o = m->o.as<bf16_t>();
-  bf16_t* y = m->y.as<bf16_t>();
-  float* P = m->P.as<float>();
+  const StepMeta meta = w.meta();
   Profiler& pf = m->prof;
   {
     Timed t(pf, st, "rope_table");
-    launch_rope_table(R, meta.pos, m->inv_freq.as<double>(), md.hd / 2, m->cos_t.as<float>(),
-                      m->sin_t.as<float>(), st);
+    launch_rope_table(R, meta.pos, m->inv_freq.as<double>(), md.hd / 2, w.cos_t, w.sin_t, st);
   }
   {
     Timed t(pf, st, "embed_norm");
-    launch_embed_norm(R, meta.tok, m->embed, m->layers[0].attn_norm, md.d, md.eps, h, u, st);
+    launch_embed_norm(R, meta.tok, m->embed, m->layers[0].attn_norm, md.d, md.eps, w.h, w.u, st);
   }
   for (int l = 0; l < m->cfg.n_layers; ++l) {
     const LayerW& L = m->layers[l];
     int s = 1;
     {
       Timed t(pf, st, "gemm_qkv");
-      gemm(m, u, md.d, nullptr, L.w_qkv, R, md.qkv, md.d, &s, st);
+      WARCHK(gemm(w, w.u, md.d, nullptr, L.w_qkv, R, md.qkv, md.d, &s, st));
     }
     {
       Timed t(pf, st, "qkv_rope_kvwrite");
-      launch_qkv_rope(R, s, P, md, m->cos_t.as<float>(), m->sin_t.as<float>(), meta, meta.row_req,
-                      p->dev.table, p->dev.max_pages, p->geom, l, q, st);
+      launch_qkv_rope(R, s, w.P, md, w.cos_t, w.sin_t, meta, meta.row_req, p->dev.table, p->dev.max_pages,
+                      p->geom, l, w.q, st);
     }
     AttnArgs a = attn_base;
     a.layer = l;
@@ -326,66 +421,91 @@ war_status run_layers(war_model* m, war_kv_pool* p, int R, const AttnArgs& attn_
       Timed t(pf, st, "attention");
       launch_attn(a, RB, md.hd, attn_grid, st);
     }
-
     {
       Timed t(pf, st, "attn_combine");
       launch_attn_combine(a, RB, md.hd, n_segs, st);
     }
     {
       Timed t(pf, st, "gemm_o");
-      gemm(m, o, md.nq * md.hd, nullptr, L.w_o, R, md.d, md.nq * md.hd, &s, st);
+      WARCHK(gemm(w, w.o, md.nq * md.hd, nullptr, L.w_o, R, md.d, md.nq * md.hd, &s, st));
     }
     {
       Timed t(pf, st, "residual_norm");
-      launch_residual_norm(R, s, P, md.d, L.ffn_norm, md.eps, h, u, st);
+      launch_residual_norm(R, s, w.P, md.d, L.ffn_norm, md.eps, w.h, w.u, st);
     }
     {
       Timed t(pf, st, "gemm_gate_up_swiglu");
-      gemm(m, u, md.d, nullptr, L.w_gate_up, R, 2 * md.F, md.d, &s, st, false, nullptr, y);
+      WARCHK(gemm(w, w.u, md.d, nullptr, L.w_gate_up, R, 2 * md.F, md.d, &s, st, false, nullptr, w.y));
     }
     {
       Timed t(pf, st, "gemm_down");
-      gemm(m, y, md.F, nullptr, L.w_down, R, md.d, md.F, &s, st);
+      WARCHK(gemm(w, w.y, md.F, nullptr, L.w_down, R, md.d, md.F, &s, st));
     }
     const bf16_t* gnext = l + 1 < m->cfg.n_layers ? m->layers[l + 1].attn_norm : m->final_norm;
     {
       Timed t(pf, st, "residual_norm");
-      launch_residual_norm(R, s, P, md.d, gnext, md.eps, h, u, st);
+      launch_residual_norm(R, s, w.P, md.d, gnext, md.eps, w.h, w.u, st);
     }
   }
   HIPCHK(hipGetLastError());
   return WAR_OK;
 }
 
-AttnArgs attn_args(war_model* m, war_kv_pool* p, int TB) {
+AttnArgs attn_args(war_model* m, const Workspace& w, war_kv_pool* p, int TB) {
   AttnArgs a{};
-  a.q = m->q.as<bf16_t>();
+  a.q = w.q;
   a.q_stride = m->md.nq * m->md.hd;
   a.kv = p->geom;
   a.table = p->dev.table;
   a.max_pages = p->dev.max_pages;
-  a.meta = m->meta();
+  a.meta = w.meta();
   a.G = m->md.nq / m->md.nkv;
   a.TB = TB;
   a.n_kv_heads = m->md.nkv;
   a.scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)m->md.hd));
-  a.pm = m->pm.as<float>();
-  a.pl = m->pl.as<float>();
-  a.po = m->po.as<float>();
-  a.o = m->o.as<bf16_t>();
-  a.unit_ctr = m->unit_ctr.as<int32_t>();
+  a.pm = w.pm;
+  a.pl = w.pl;
+  a.po = w.po;
+  a.o = w.o;
+  a.unit_ctr = w.unit_ctr;
   return a;
 }
 
-war_status ensure_items(war_model* m, int64_t n_items, int RB) {
-  HIPCHK(m->items.ensure(std::max<int64_t>(n_items, 1) * sizeof(int4)));
-  HIPCHK(m->udesc.ensure(std::max<int64_t>(n_items, 1) * 2 * sizeof(int4)));
-  HIPCHK(m->order.ensure(std::max<int64_t>(n_items, 1) * sizeof(int32_t)));
-  const int64_t pr = std::max<int64_t>(n_items, 1) * m->md.nkv * RB;
-  HIPCHK(m->pm.ensure(pr * sizeof(float)));
-  HIPCHK(m->pl.ensure(pr * sizeof(float)));
-  HIPCHK(m->po.ensure(pr * m->md.hd * sizeof(float)));
+// Grow the model's own workspace to hold n_items attention items of RB rows
+// (rows: max_rows; partials: kPartialCap or what max_rows needs).  A new
+// allocation starts with the attention work counters at zero.
+war_status ensure_ws(war_model* m, int64_t n_items, int RB) {
+  Workspace& w = m->ws;
+  if (w.R && n_items <= w.items_cap && RB <= w.rb_cap) return WAR_OK;
+  const int64_t items = std::max<int64_t>(n_items, w.items_cap);
+  const int rb = std::max(RB, w.rb_cap);
+  const int64_t pel = std::max<int64_t>(kPartialCap, partials_needed(m->md, m->max_rows));
+  const size_t bytes = ws_layout(m->md, m->max_rows, items, rb, pel, nullptr, nullptr);
+  const bool tree = w.tree_step;
+  HIPCHK(m->ws_buf.ensure(bytes));
+  ws_layout(m->md, m->max_rows, items, rb, pel, m->ws_buf.as<char>(), &w);
+  w.tree_step = tree;
+  HIPCHK(hipMemset(w.unit_ctr, 0, 8 * 4));
   return WAR_OK;
+}
+
+// ---- host lower bound of the pool's free pages (see war_kv_pool)
+void set_exact_free(war_kv_pool* p, int64_t fc) {
+  p->base_fc = fc;
+  p->base_total = p->total_need;
+  p->base_seq = p->commit_issued;
+}
+
+int64_t free_lower_bound(war_kv_pool* p) {
+  int64_t lb = p->base_fc - (p->total_need - p->base_total);
+  const unsigned long long r = __atomic_load_n(p->report, __ATOMIC_ACQUIRE);
+  const uint32_t seq = (uint32_t)(r >> 32);
+  const int64_t fc = (int64_t)(uint32_t)r;
+  // a commit newer than the exact count, still in the ring
+  if ((int32_t)(seq - p->base_seq) > 0 && (int32_t)(p->commit_issued - seq) >= 0 &&
+      p->commit_issued - seq < (uint32_t)kRing)
+    lb = std::max(lb, fc - (p->total_need - p->need_at[seq % kRing]));
+  return lb;
 }
 
 // Read the pool's device scalars (syncs the stream).
@@ -395,7 +515,7 @@ war_status read_free_count(war_kv_pool* p, hipStream_t st, int32_t* fc, int32_t*
   HIPCHK(hipStreamSynchronize(st));
   *fc = sc[0];
   if (err) *err = sc[1];
-  p->free_lb = sc[0];
+  set_exact_free(p, sc[0]);
   return WAR_OK;
 }
 
@@ -501,33 +621,8 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
     war_model_destroy(m);
     return fail(WAR_ERR_HIP, std::string("weight copy: ") + hipGetErrorString(e0));
   }
-  const int R = cfg->max_rows;
-  m->max_rows = R;
-  m->n_req_cap = std::max(R, kMaxBatch);
-  m->n_seg_cap = R + kMaxBatch;
-  const size_t wide = std::max({md.d, md.F, md.nq * md.hd});
-  hipError_t e = hipSuccess;
-  auto ok = [&](hipError_t x) { if (e == hipSuccess) e = x; };
-  ok(m->h.ensure((size_t)R * md.d * 4));
-  ok(m->u.ensure((size_t)R * wide * 2));
-  ok(m->q.ensure((size_t)R * md.nq * md.hd * 2));
-  ok(m->o.ensure((size_t)R * md.nq * md.hd * 2));
-  ok(m->y.ensure((size_t)R * md.F * 2));
-  const int64_t pneed = std::max<int64_t>((int64_t)R * std::max(md.qkv, 2 * md.F), 1);
-  ok(m->P.ensure((size_t)std::max(kPartialCap, pneed) * 4));
-  ok(m->cos_t.ensure((size_t)R * md.hd / 2 * 4));
-  ok(m->sin_t.ensure((size_t)R * md.hd / 2 * 4));
-  ok(m->inv_freq.ensure((size_t)md.hd / 2 * 8));
-  ok(m->amax_v.ensure((size_t)R * (md.V / 128) * 4));
-  ok(m->amax_i.ensure((size_t)R * (md.V / 128) * 4));
-  ok(m->rows_i32.ensure((size_t)4 * R * 4));
-  ok(m->tree_i32.ensure((size_t)2 * R * 4));
-  ok(m->reqs_i32.ensure((size_t)4 * m->n_req_cap * 4));
-  ok(m->segs_i32.ensure((size_t)4 * m->n_seg_cap * 4));
-  ok(m->n_items.ensure(16));
-  ok(m->a_rows.ensure((size_t)kMaxBatch * 4));
-  ok(m->unit_ctr.ensure(8 * 4));
-  if (e == hipSuccess) e = hipMemset(m->unit_ctr.p, 0, m->unit_ctr.bytes);
+  m->max_rows = cfg->max_rows;
+  hipError_t e = m->inv_freq.ensure((size_t)md.hd / 2 * 8);
   if (e == hipSuccess) {
     std::vector<double> inv(md.hd / 2);
     for (int j = 0; j < md.hd / 2; ++j) inv[j] = std::pow((double)cfg->rope_base, -2.0 * j / md.hd);
@@ -537,15 +632,18 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
     war_model_destroy(m);
     return fail(WAR_ERR_HIP, std::string("workspace allocation: ") + hipGetErrorString(e));
   }
+  if (war_status ws = ensure_ws(m, 1, 16); ws != WAR_OK) {
+    const std::string msg = g_err;
+    war_model_destroy(m);
+    return fail(ws, msg);
+  }
   *out = m;
   return WAR_OK;
 }
 
 void war_model_destroy(war_model* m) {
   if (!m) return;
-  for (DevBuf* b : {&m->wts, &m->h, &m->u, &m->q, &m->o, &m->y, &m->P, &m->cos_t, &m->sin_t, &m->inv_freq,
-                    &m->amax_v, &m->amax_i, &m->rows_i32, &m->tree_i32, &m->path_ws, &m->reqs_i32, &m->segs_i32, &m->n_items,
-                    &m->items, &m->order, &m->udesc, &m->unit_ctr, &m->logits_ws, &m->row_out, &m->pm, &m->pl, &m->po, &m->a_rows, &m->stage_dev})
+  for (DevBuf* b : {&m->wts, &m->inv_freq, &m->ws_buf, &m->path_ws, &m->logits_ws, &m->row_out, &m->stage_dev})
     b->release();
   if (m->pinned) (void)hipHostFree(m->pinned);
   for (hipEvent_t e : m->prof.pool) (void)hipEventDestroy(e);
@@ -588,7 +686,20 @@ war_status war_kv_pool_create(const war_model_config* cfg, void* kv_pages, int32
   p->dev.max_seqs = max_seqs;
   p->dev.max_pages = max_pages_per_seq;
   p->dev.page_size = cfg->page_size;
-  p->free_lb = num_pages;
+  // the commit kernel's report word: pinned, mapped into the device's address space
+  e = hipHostMalloc(reinterpret_cast<void**>(&p->report), sizeof(unsigned long long),
+                    hipHostMallocMapped | hipHostMallocCoherent);
+  if (e == hipSuccess) {
+    *p->report = (unsigned long long)(uint32_t)num_pages;  // commit 0, every page free
+    e = hipHostGetDevicePointer(reinterpret_cast<void**>(&p->dev.report), p->report, 0);
+  } else {
+    p->report = nullptr;
+  }
+  if (e != hipSuccess) {
+    war_kv_pool_destroy(p);
+    return fail(WAR_ERR_HIP, std::string("pool report word: ") + hipGetErrorString(e));
+  }
+  p->base_fc = num_pages;
   launch_pool_init(p->dev, st);
   e = hipGetLastError();
   if (e != hipSuccess) {
@@ -604,6 +715,7 @@ void war_kv_pool_destroy(war_kv_pool* p) {
   p->state.release();
   p->tmp.release();
   if (p->pinned) (void)hipHostFree(p->pinned);
+  if (p->report) (void)hipHostFree(p->report);
   delete p;
 }
 
@@ -619,10 +731,15 @@ war_status war_pool_state(war_kv_pool* p, int32_t* free_count, int32_t* free_sta
   if (refcount) HIPCHK(hipMemcpy(refcount, p->dev.refcount, (size_t)p->dev.num_pages * 4, hipMemcpyDeviceToHost));
   if (held) HIPCHK(hipMemcpy(held, p->dev.held, (size_t)p->dev.max_seqs * 4, hipMemcpyDeviceToHost));
   if (step_base) HIPCHK(hipMemcpy(step_base, p->dev.base, (size_t)p->dev.max_seqs * 4, hipMemcpyDeviceToHost));
-  if (err)
+  if (err) {
+    // reported once: the flags start again from zero
+    HIPCHK(hipMemsetAsync(p->dev.scalars + 1, 0, 4, st));
+    HIPCHK(hipStreamSynchronize(st));
     return fail(WAR_ERR_DEVICE, err & ERR_NO_PAGES     ? "device page shortage"
+                                : err & ERR_DUP_SEQ    ? "a sequence id appears twice in one verify step"
                                 : err & ERR_BAD_PARENT ? "tree parent out of range on device"
-                                                       : "bad token id or context length on device");
+                                                       : "bad token id, sequence id or context length on device");
+  }
   return WAR_OK;
 }
 
@@ -643,14 +760,13 @@ war_status war_kv_alloc(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host, 
     CHECK(pg <= p->dev.max_pages, "n_tokens exceeds max_pages_per_seq");
     bound += pg;
   }
-  int64_t need = bound;
-  if (bound > p->free_lb) {
+  if (bound > free_lower_bound(p)) {
     int32_t fc;
     s = read_free_count(p, st, &fc, nullptr);
     if (s != WAR_OK) return s;
     std::vector<int32_t> held(p->dev.max_seqs);
     HIPCHK(hipMemcpy(held.data(), p->dev.held, held.size() * 4, hipMemcpyDeviceToHost));
-    need = 0;
+    int64_t need = 0;
     for (int i = 0; i < n; ++i)
       need += std::max(0, cdiv_i(n_tokens_host[i], p->dev.page_size) - held[seq_ids_host[i]]);
     if (need > fc) return fail(WAR_ERR_OUT_OF_PAGES, "not enough free KV pages");
@@ -660,9 +776,8 @@ war_status war_kv_alloc(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host, 
   const int32_t* d = p->tmp.as<int32_t>();
   launch_grow(p->dev, n, d, d + n, nullptr, 0, st);
   HIPCHK(hipGetLastError());
-  HIPCHK(hipStreamSynchronize(st));  // the pinned staging buffer is reused
-  p->free_lb -= need;
-  return WAR_OK;
+  int32_t fc;
+  return read_free_count(p, st, &fc, nullptr);  // waits: the pinned staging buffer is reused
 }
 
 war_status war_kv_fork(war_kv_pool* p, int32_t src_seq, int32_t dst_seq, int32_t n_tokens, void* stream) {
@@ -682,7 +797,8 @@ war_status war_kv_fork(war_kv_pool* p, int32_t src_seq, int32_t dst_seq, int32_t
   launch_fork(p->dev, src_seq, dst_seq, npg, st);
   HIPCHK(hipGetLastError());
   if (npg > 0) p->forked = true;
-  return WAR_OK;
+  int32_t fc;
+  return read_free_count(p, st, &fc, nullptr);
 }
 
 war_status war_kv_free(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host, void* stream) {
@@ -698,8 +814,8 @@ war_status war_kv_free(war_kv_pool* p, int32_t n, const int32_t* seq_ids_host, v
   if (s != WAR_OK) return s;
   launch_free(p->dev, n, p->tmp.as<int32_t>(), st);
   HIPCHK(hipGetLastError());
-  HIPCHK(hipStreamSynchronize(st));
-  return WAR_OK;
+  int32_t fc;
+  return read_free_count(p, st, &fc, nullptr);  // waits: the pinned staging buffer is reused
 }
 
 war_status war_kv_load(war_kv_pool* p, int32_t seq_id, int32_t layer, int32_t pos0, int32_t n,
@@ -730,11 +846,19 @@ struct SampleParams {
   int top_k = 1;
 };
 
+// A fixed device region to lay the step's workspace over instead of the
+// model's own workspace (which grows on demand); nothing is allocated then.
+struct StaticWs {
+  char* base;
+  size_t bytes;
+};
+
 war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
                        const int32_t* ctx_lens, const int32_t* last_tokens, const int32_t* draft_tokens,
                        const int32_t* draft_lens, int32_t k_max, int32_t* accept_lens,
                        int32_t* next_tokens, float* logits, void* stream, const SampleParams& sp,
-                       const int32_t* draft_parents = nullptr, int32_t* accept_path = nullptr) {
+                       const int32_t* draft_parents = nullptr, int32_t* accept_path = nullptr,
+                       const StaticWs* fixed = nullptr) {
   CHECK(m && p, "null model or pool");
   CHECK(same_shape(m->cfg, p->cfg), "model and pool shapes differ");
   CHECK(!p->pending, "previous verify step not committed");
@@ -751,14 +875,49 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
   if (tree && k_max + 1 > 32) return fail(WAR_ERR_UNSUPPORTED, "tree drafts: k_max + 1 must be <= 32");
   if (tree && sp.uniforms) return fail(WAR_ERR_UNSUPPORTED, "tree drafts are verified greedily");
 
+  const int kp1 = k_max + 1;
+  const int R = B * kp1;
+  const int RB = attn_rows_per_block(G, kp1);
+  // keys per attention item: long enough that each wave streams 8+ blocks
+  int chunk = 1024;
+  while (cdiv_i(p->dev.max_pages * P, chunk) > kMaxItemsPerSeq) chunk *= 2;
+  int64_t max_items = (int64_t)B * cdiv_i(p->dev.max_pages * P, chunk);
+  Workspace wsv;
+  if (fixed) {
+    // a fixed region: rows exactly R; the attention items bound shrinks by
+    // longer chunks until the layout fits (the step setup may still double it)
+    const int64_t pel = partials_needed(m->md, R);
+    size_t bytes = ws_layout(m->md, R, max_items, RB, pel, nullptr, nullptr);
+    while (bytes > fixed->bytes && chunk < (1 << 20)) {
+      chunk *= 2;
+      max_items = (int64_t)B * cdiv_i(p->dev.max_pages * P, chunk);
+      bytes = ws_layout(m->md, R, max_items, RB, pel, nullptr, nullptr);
+    }
+    if (bytes > fixed->bytes)
+      return fail(WAR_ERR_UNSUPPORTED, "the step's workspace (" + std::to_string(bytes) +
+                                           " bytes) exceeds the fixed region (" +
+                                           std::to_string(fixed->bytes) + " bytes)");
+    ws_layout(m->md, R, max_items, RB, pel, fixed->base, &wsv);
+  } else {
+    war_status s = ensure_ws(m, max_items, RB);
+    if (s != WAR_OK) return s;
+    wsv = m->ws;
+  }
+  wsv.tree_step = tree;
+  if (!fixed) m->ws.tree_step = tree;
+  const Workspace& w = wsv;
+
   // capacity: ctx + draft + 1 slots need at most cdiv(k_max+1, P) new pages per request
   const int64_t bound = (int64_t)B * cdiv_i(k_max + 1, P);
   int64_t need = bound;
-  if (bound > p->free_lb) {
+  if (bound > free_lower_bound(p)) {
     int32_t fc;
+    ++p->exact_waits;
     war_status s = read_free_count(p, st, &fc, nullptr);
     if (s != WAR_OK) return s;
     if (bound > fc) {
+      // with a fixed region no per-request state is read (it would need host buffers)
+      if (fixed) return fail(WAR_ERR_OUT_OF_PAGES, "fewer free KV pages than B * ceil((k_max+1)/page_size)");
       std::vector<int32_t> sid(B), ctx(B), dl(B, k_max), held(p->dev.max_seqs);
       HIPCHK(hipMemcpy(sid.data(), seq_ids, B * 4, hipMemcpyDeviceToHost));
       HIPCHK(hipMemcpy(ctx.data(), ctx_lens, B * 4, hipMemcpyDeviceToHost));
@@ -774,20 +933,11 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
     }
   }
 
-  const int kp1 = k_max + 1;
-  const int R = B * kp1;
-  const int RB = attn_rows_per_block(G, kp1);
-  // keys per attention item: long enough that each wave streams 8+ blocks
-  int chunk = 1024;
-  while (cdiv_i(p->dev.max_pages * P, chunk) > kMaxItemsPerSeq) chunk *= 2;
-  const int64_t max_items = (int64_t)B * cdiv_i(p->dev.max_pages * P, chunk);
-  war_status s = ensure_items(m, max_items, RB);
-  if (s != WAR_OK) return s;
-
   VerifySetupArgs va;
   va.B = B;
   va.k_max = k_max;
   va.vocab = m->md.V;
+  va.unit_ctr = w.unit_ctr;
   va.chunk = chunk;
   va.items_double = cdiv_i(2 * kAttnGrid, m->md.nkv);  // 2+ units per workgroup of a full grid
   va.seq_ids = seq_ids;
@@ -799,21 +949,21 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
   va.rb = RB;
   va.cascade = p->forked && B > 1 ? 1 : 0;  // shared-prefix units for forked siblings
   va.draft_parents = tree ? draft_parents : nullptr;
-  m->tree_step = tree;
   if (tree && !accept_path) {
     HIPCHK(m->path_ws.ensure((size_t)B * k_max * 4));
     accept_path = m->path_ws.as<int32_t>();
   }
+  const StepMeta meta = w.meta();
   {
     Timed t(m->prof, st, "verify_setup");
-    launch_verify_setup(p->dev, va, m->meta(), st);
+    launch_verify_setup(p->dev, va, meta, st);
   }
 
-  AttnArgs a = attn_args(m, p, kp1);
+  AttnArgs a = attn_args(m, w, p, kp1);
   a.prb = RB;
   // persistent grid = resident capacity: 2 workgroups per CU
   const int grid = (int)std::min<int64_t>(max_items * m->md.nkv, kAttnGrid);
-  s = run_layers(m, p, R, a, RB, grid, B, st);
+  war_status s = run_layers(m, w, p, R, a, RB, grid, B, st);
   if (s != WAR_OK) return s;
   int sdummy;
   if (sp.uniforms) {
@@ -826,12 +976,12 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
     HIPCHK(m->row_out.ensure((size_t)R * 3 * 4));
     {
       Timed t(m->prof, st, "gemm_lm_head");
-      gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, R, m->md.V, m->md.d, &sdummy, st, true, lg);
+      WARCHK(gemm(w, w.u, m->md.d, nullptr, m->w_lm, R, m->md.V, m->md.d, &sdummy, st, true, lg));
     }
     SampleArgs sa{};
     sa.logits = lg;
     sa.V = m->md.V;
-    sa.ntok = m->meta().req_ntok;
+    sa.ntok = meta.req_ntok;
     sa.drafts = draft_tokens;
     sa.k_max = k_max;
     sa.kp1 = kp1;
@@ -845,21 +995,19 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
   } else {
     {
       Timed t(m->prof, st, "gemm_lm_head_argmax");
-      gemm(m, m->u.as<bf16_t>(), m->md.d, nullptr, m->w_lm, R, m->md.V, m->md.d, &sdummy,
-           st, true, logits);
+      WARCHK(gemm(w, w.u, m->md.d, nullptr, m->w_lm, R, m->md.V, m->md.d, &sdummy, st, true, logits));
     }
     Timed t(m->prof, st, "argmax_accept");
-    launch_argmax_accept(B, m->meta().req_ntok, kp1, m->md.V / 128, m->amax_v.as<float>(),
-                         m->amax_i.as<int32_t>(), draft_tokens, tree ? draft_parents : nullptr, k_max,
-                         accept_lens, next_tokens, accept_path, st);
+    launch_argmax_accept(B, meta.req_ntok, kp1, m->md.V / 128, w.amax_v, w.amax_i, draft_tokens,
+                         tree ? draft_parents : nullptr, k_max, accept_lens, next_tokens, accept_path, st);
   }
   if (tree) {
     Timed t(m->prof, st, "kv_compact");
-    launch_kv_compact(p->geom, m->cfg.n_layers, B, m->meta(), p->dev.table, p->dev.max_pages, accept_lens,
+    launch_kv_compact(p->geom, m->cfg.n_layers, B, meta, p->dev.table, p->dev.max_pages, accept_lens,
                       accept_path, k_max, st);
   }
   HIPCHK(hipGetLastError());
-  p->free_lb -= need;
+  p->total_need += need;
   p->pending = true;
   p->pending_B = B;
   return WAR_OK;
@@ -910,8 +1058,11 @@ war_status war_kv_commit(war_kv_pool* p, int32_t B, const int32_t* seq_ids, int3
   CHECK(p->pending, "no verify step to commit");
   CHECK(B == p->pending_B, "B differs from the verify step's");
   CHECK(seq_ids && ctx_lens && accept_lens, "null array");
-  launch_commit(p->dev, B, seq_ids, ctx_lens, accept_lens, static_cast<hipStream_t>(stream));
+  const uint32_t seq = p->commit_issued + 1;
+  launch_commit(p->dev, B, seq_ids, ctx_lens, accept_lens, seq, static_cast<hipStream_t>(stream));
   HIPCHK(hipGetLastError());
+  p->commit_issued = seq;
+  p->need_at[seq % kRing] = p->total_need;
   p->pending = false;
   return WAR_OK;
 }
@@ -927,7 +1078,6 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
   hipStream_t st = static_cast<hipStream_t>(stream);
   const int P = p->dev.page_size;
   const int G = m->md.nq / m->md.nkv;
-  m->tree_step = false;  // prefill rows are a causal chain
   int64_t total = 0;
   for (int i = 0; i < n; ++i) {
     CHECK(n_new_host[i] >= 1, "n_new must be >= 1");
@@ -965,7 +1115,7 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
   HIPCHK(hipMemcpyAsync(d_new, m->pinned, n * 4, hipMemcpyHostToDevice, st));
   launch_grow(p->dev, n, seq_ids, ctx_lens, d_new, 1, st);
   HIPCHK(hipGetLastError());
-  p->free_lb = fc - need;
+  set_exact_free(p, fc - need);
 
   // forward over chunks of at most max_rows packed rows
   const int RB = 48;
@@ -1022,13 +1172,15 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
         }
     }
     const int nseg = (int)sg_b.size();
-    CHECK(nseg <= m->n_seg_cap && nr <= m->n_req_cap, "internal: prefill chunk too fragmented");
+    CHECK(nseg <= m->ws.n_seg_cap && nr <= m->ws.n_req_cap, "internal: prefill chunk too fragmented");
     // previous chunk's kernels read the metadata buffers: wait before overwriting
-    // (and before ensure_items may reallocate the work list)
+    // (and before ensure_ws may reallocate the workspace)
     HIPCHK(hipStreamSynchronize(st));
-    s = ensure_items(m, (int64_t)items.size(), RB);
+    s = ensure_ws(m, (int64_t)items.size(), RB);
     if (s != WAR_OK) return s;
-    const StepMeta meta = m->meta();  // after any reallocation
+    m->ws.tree_step = false;  // prefill rows are a causal chain
+    const Workspace& w = m->ws;
+    const StepMeta meta = w.meta();  // after any reallocation
     auto h2d = [&](void* dst, const void* src, size_t bytes) {
       return hipMemcpyAsync(dst, src, bytes, hipMemcpyHostToDevice, st);
     };
@@ -1052,11 +1204,11 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
     HIPCHK(h2d(meta.n_items, ni4, 16));
     HIPCHK(hipStreamSynchronize(st));  // host vectors go out of scope below
 
-    AttnArgs a = attn_args(m, p, TB);
+    AttnArgs a = attn_args(m, w, p, TB);
     a.meta.order = nullptr;  // prefill items run in list order
     a.prb = RB;
     const int grid = (int)std::min<int64_t>((int64_t)ni * m->md.nkv, kAttnGrid);
-    s = run_layers(m, p, R, a, RB, std::max(grid, 1), nseg, st);
+    s = run_layers(m, w, p, R, a, RB, std::max(grid, 1), nseg, st);
     if (s != WAR_OK) return s;
     // LM head on the rows that end a sequence inside this chunk
     std::vector<int32_t> last_rows;
@@ -1070,20 +1222,19 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
     }
     if (!last_rows.empty()) {
       const int nl = (int)last_rows.size();
-      HIPCHK(hipMemcpyAsync(m->a_rows.p, last_rows.data(), nl * 4, hipMemcpyHostToDevice, st));
+      HIPCHK(hipMemcpyAsync(w.a_rows, last_rows.data(), nl * 4, hipMemcpyHostToDevice, st));
       int sd;
-      gemm(m, m->u.as<bf16_t>(), m->md.d, m->a_rows.as<int32_t>(), m->w_lm, nl, m->md.V,
-           m->md.d, &sd, st, true, last_logits ? last_logits + (int64_t)first_seq * m->md.V : nullptr);
-      launch_argmax_accept(nl, nullptr, 1, m->md.V / 128, m->amax_v.as<float>(), m->amax_i.as<int32_t>(),
-                           nullptr, nullptr, 0, nullptr, next_tokens + first_seq, nullptr, st);
+      WARCHK(gemm(w, w.u, m->md.d, w.a_rows, m->w_lm, nl, m->md.V, m->md.d, &sd, st, true,
+                  last_logits ? last_logits + (int64_t)first_seq * m->md.V : nullptr));
+      launch_argmax_accept(nl, nullptr, 1, m->md.V / 128, w.amax_v, w.amax_i, nullptr, nullptr, 0, nullptr,
+                           next_tokens + first_seq, nullptr, st);
       HIPCHK(hipGetLastError());
       HIPCHK(hipStreamSynchronize(st));  // last_rows goes out of scope
     }
   }
   launch_add_ctx(n, ctx_lens, d_new, st);
   HIPCHK(hipGetLastError());
-  HIPCHK(hipStreamSynchronize(st));
-  return WAR_OK;
+  return read_free_count(p, st, &fc, nullptr);  // waits for the whole append
 }
 
 war_status war_profile(war_model* m, int32_t enable) {
@@ -1152,18 +1303,36 @@ war_status war_debug_sample(const float* logits, int32_t V, int32_t B, int32_t k
   return WAR_OK;
 }
 
+war_status war_debug_pool_waits(war_kv_pool* p, int64_t* waits) {
+  CHECK(p && waits, "null argument");
+  *waits = p->exact_waits;
+  return WAR_OK;
+}
+
 war_status war_debug_workspace(war_model* m, const char* name, void** ptr, int64_t* bytes) {
   CHECK(m && name && ptr && bytes, "null argument");
   const std::string n(name);
-  const DevBuf* b = n == "h" ? &m->h : n == "u" ? &m->u : n == "q" ? &m->q : n == "o" ? &m->o
-                  : n == "P" ? &m->P : n == "pm" ? &m->pm : n == "pl" ? &m->pl : n == "po" ? &m->po
-                  : n == "rows" ? &m->rows_i32 : n == "reqs" ? &m->reqs_i32 : n == "items" ? &m->items
-                  : n == "order" ? &m->order : n == "n_items" ? &m->n_items
-                  : n == "tree" ? &m->tree_i32 : nullptr;
-  CHECK(b, "unknown workspace buffer");
-  *ptr = b->p;
-  *bytes = (int64_t)b->bytes;
-  return WAR_OK;
+  const Workspace& w = m->ws;
+  const ModelDims& md = m->md;
+  const int64_t R = w.R, nqhd = (int64_t)md.nq * md.hd, pr = w.items_cap * md.nkv * w.rb_cap;
+  struct Entry {
+    const char* name;
+    const void* p;
+    int64_t bytes;
+  };
+  const Entry table[] = {
+      {"h", w.h, R * md.d * 4}, {"u", w.u, R * md.d * 2}, {"q", w.q, R * nqhd * 2}, {"o", w.o, R * nqhd * 2},
+      {"P", w.P, w.p_elems * 4}, {"pm", w.pm, pr * 4}, {"pl", w.pl, pr * 4}, {"po", w.po, pr * md.hd * 4},
+      {"rows", w.rows, 4 * R * 4}, {"reqs", w.reqs, 4 * (int64_t)w.n_req_cap * 4},
+      {"items", w.items, w.items_cap * 16}, {"order", w.order, w.items_cap * 4}, {"n_items", w.n_items, 16},
+      {"tree", w.tree, 2 * R * 4}};
+  for (const Entry& e : table)
+    if (n == e.name) {
+      *ptr = const_cast<void*>(e.p);
+      *bytes = e.bytes;
+      return WAR_OK;
+    }
+  return fail(WAR_ERR_INVALID_ARG, "unknown workspace buffer");
 }
 
 }  // extern "C"

@@ -27,8 +27,8 @@ EXPORTS = ["war_weight_count", "war_model_create", "war_model_destroy", "war_kv_
            "war_kv_pool_destroy", "war_kv_alloc", "war_kv_fork", "war_kv_free", "war_kv_load",
            "war_prefill_append", "war_verify_step", "war_verify_step_sampled", "war_verify_step_tree",
            "war_kv_commit", "war_pool_state",
-           "war_last_error", "war_debug_mfma16", "war_debug_workspace", "war_debug_sample", "war_profile",
-           "war_profile_read"]
+           "war_last_error", "war_debug_mfma16", "war_debug_workspace", "war_debug_sample",
+           "war_debug_pool_waits", "war_profile", "war_profile_read"]
 
 
 class WarError(RuntimeError):
@@ -70,6 +70,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         "war_debug_sample": (i32, [vp, i32, i32, i32, vp, vp, vp, C.c_float, i32, vp, vp, vp]),
         "war_debug_mfma16": (i32, [vp, vp, vp, vp]),
         "war_debug_workspace": (i32, [vp, C.c_char_p, C.POINTER(vp), C.POINTER(C.c_int64)]),
+        "war_debug_pool_waits": (i32, [vp, C.POINTER(C.c_int64)]),
         "war_profile": (i32, [vp, i32]),
         "war_profile_read": (i32, [vp, C.c_char_p, i32]),
     }
@@ -201,6 +202,12 @@ class Pool:
                "held": np.array(held[:], np.int32), "base": np.array(base[:], np.int32),
                "table": self.block_tables.cpu().numpy(), "status": st}
         return out
+
+    def waits(self) -> int:
+        """Verify steps that waited to read the exact free page count."""
+        n = C.c_int64()
+        _check(lib().war_debug_pool_waits(self.handle, C.byref(n)))
+        return n.value
 
     def close(self):
         if getattr(self, "handle", None):
