@@ -10,9 +10,13 @@ computed in the test from the oracle alone (fp32_drift_tol).
 
 Integers decided by floating point (greedy tokens, accept lengths, next
 tokens): bit-exact, except where the oracle's top-2 logit gap is below 0.1
-(a near-tie), which is reported instead of failed.  A mismatch at a row whose
-oracle gap exceeds twice the row's measured max |logit error| is always a
-failure: with every logit within half the gap, the argmax cannot change.
+(a near-tie), which is reported instead of failed.  A flip at a row whose
+oracle gap is 0.1 or more always fails, and so does one whose gap exceeds
+twice the row's measured max |logit error| (with every logit within half the
+gap the argmax cannot change).  At full depth the logit error can exceed
+0.05, so rows whose gap lies in [0.1, 2 x row error) could flip without
+breaking the arithmetic: they are counted ("band") and reported, and a flip
+there still fails.
 """
 from __future__ import annotations
 
@@ -45,21 +49,29 @@ def compare_request(o_logits: np.ndarray, g_logits: np.ndarray, drafts, o_accept
     g_greedy = argmax_lowest(g_logits[: n + 1])
     o_greedy = argmax_lowest(o_logits[: n + 1])
     row_err = d.max(axis=1)
+    flips = 0
+    band = int(((gap >= NEAR_TIE) & (gap < 2 * row_err)).sum())
+    if band:
+        report.append(f"{tag}: {band} row(s) with oracle gap in [0.1, 2 x row error)")
     for i in range(n + 1):
         if g_greedy[i] != o_greedy[i]:
+            assert gap[i] < NEAR_TIE, \
+                f"{tag}: row {i} argmax differs at oracle gap {gap[i]:.4g} >= {NEAR_TIE}"
             assert gap[i] <= 2 * row_err[i] + 1e-6, \
                 f"{tag}: row {i} argmax differs although every logit is within half the gap " \
                 f"(gap {gap[i]:.4g}, row err {row_err[i]:.3g})"
+            flips += 1
             report.append(f"{tag}: row {i} near-tie, oracle gap {gap[i]:.3g}")
     # the GPU's own acceptance must follow from its greedy rows
     from oracle.accept import accept_length
     a = accept_length(drafts, g_greedy)
     assert (g_accept, g_next) == (a, int(g_greedy[a])), f"{tag}: GPU accept/next inconsistent"
+    same = (g_accept, g_next) == (o_accept, o_next)
     if (g_greedy[: n + 1] == o_greedy[: n + 1]).all():
-        assert (g_accept, g_next) == (o_accept, o_next), f"{tag}: accept/next differ from the oracle"
-    else:
+        assert same, f"{tag}: accept/next differ from the oracle"
+    elif not same:
         report.append(f"{tag}: accept/next ({g_accept},{g_next}) vs oracle ({o_accept},{o_next}) at a near-tie")
-    return {"err": err, "min_gap": float(gap.min())}
+    return {"err": err, "min_gap": float(gap.min()), "band": band, "flips": flips, "same": same}
 
 
 def shared_units(rows, rb):
@@ -107,6 +119,7 @@ def compare_tree_request(o: Dict, g_logits: np.ndarray, tokens, parents, g_accep
     row_err = d.max(axis=1)
     for i in range(n + 1):
         if g_greedy[i] != o_greedy[i]:
+            assert gap[i] < NEAR_TIE, f"{tag}: node {i} argmax differs at oracle gap {gap[i]:.4g} >= {NEAR_TIE}"
             assert gap[i] <= 2 * row_err[i] + 1e-6, \
                 f"{tag}: node {i} argmax differs although every logit is within half the gap"
             report.append(f"{tag}: node {i} near-tie, oracle gap {gap[i]:.3g}")

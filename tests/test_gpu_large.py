@@ -440,3 +440,62 @@ def test_full_size_high_load_k2_sampled():
         drafts[b] = d
     st = harness.Step(st.seq_ids, st.ctx_lens, st.last_tokens, drafts, 2)
     _full_size_check(st, 5, sample, "high_load_k2")
+
+
+def test_full_size_prefill_append():
+    """The append at full depth: two trajectories with 4000 and 4111 cached
+    tokens (seeded keys and values) each receive 64 new tokens through
+    war_prefill_append (36 layers).  The last row's logits and next token, and
+    the appended keys and values of the first, a middle and the last layer,
+    are compared with the oracle's float64 forward over the same 64 tokens.
+    The logit bound is max(5e-2, 1.5 x the drift of the oracle's fp32-
+    accumulation mode), measured on trajectory 0 (the KV bound likewise, never
+    below 3e-2)."""
+    from oracle.accept import argmax_lowest, top2_gap
+    from parity import NEAR_TIE
+    war = _war()
+    cfg = synth.LARGE
+    w = harness.large_weights(cfg)
+    model = war.Model(cfg, w, max_rows=1024)
+    ctxs = np.array([4000, 4111], np.int32)
+    n_new = [64, 64]
+    kv_seed = 5
+    pool = harness.make_pool(cfg, ctxs + 64, 8)
+    harness.load_contexts(pool, cfg, ctxs, [0, 1], kv_seed)
+    toks = [synth.uniform_tokens(80 + b, 64, cfg.vocab) for b in range(2)]
+    t = lambda a: torch.as_tensor(np.asarray(a), dtype=torch.int32).cuda()
+    ctx_d, nxt = t(ctxs), t([0, 0])
+    last = torch.zeros((2, cfg.vocab), device="cuda")
+    war.prefill_append(model, pool, t([0, 1]), ctx_d, n_new, t(np.concatenate(toks)), nxt, last)
+    torch.cuda.synchronize()
+    assert ctx_d.cpu().tolist() == (ctxs + 64).tolist()
+    gl, gn = last.cpu().numpy(), nxt.cpu().numpy()
+    W = Weights(cfg, w, cache=False)
+    layers = (0, 17, 35)
+    got = {(b, l): pool.gather_kv(b, int(ctxs[b]) + 64, l)[:, :, int(ctxs[b]):].double().cpu().numpy()
+           for b in range(2) for l in layers}
+    tol = kv_tol = None
+    report, out = [], []
+    for b in range(2):
+        kv_get = _oracle_kv_stream(cfg, kv_seed, b, int(ctxs[b]), f"append traj {b}")
+        o64, kv64 = forward_block(cfg, W, [int(x) for x in toks[b]], int(ctxs[b]), kv_get)
+        if tol is None:
+            o32, kv32 = forward_block(cfg, W, [int(x) for x in toks[b]], int(ctxs[b]), kv_get, precision="fp32")
+            tol = fp32_drift_tol(o64[-1:], o32[-1:])
+            kv_tol = max(3e-2, 1.5 * max(float(np.abs(kv64[l][i] - kv32[l][i]).max())
+                                         for l in layers for i in (0, 1)))
+        err = float(np.abs(gl[b] - o64[-1]).max())
+        assert err <= tol, (b, err, tol)
+        g = int(argmax_lowest(o64[-1:])[0])
+        if int(gn[b]) != g:
+            gap = float(top2_gap(o64[-1:])[0])
+            assert gap < NEAR_TIE, (b, int(gn[b]), g, gap)
+            report.append(f"traj {b}: next {int(gn[b])} vs {g} at gap {gap:.3g}")
+        kv_err = 0.0
+        for l in layers:
+            for i in (0, 1):
+                e = float(np.abs(got[(b, l)][i] - kv64[l][i]).max())
+                assert e <= kv_tol, (b, l, i, e, kv_tol)
+                kv_err = max(kv_err, e)
+        out.append((b, round(err, 4), round(tol, 4), round(kv_err, 4), round(kv_tol, 4)))
+    print(f"\nappend at full depth: (traj, logit err, bound, kv err, kv bound) {out}; {report}")
