@@ -1,7 +1,7 @@
 #!/usr/bin/env python3
 """Benchmark of the speculative-verification decode step on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload low_load|high_load|high_load_k2|multi_turn]
+    python bench.py [--steps K] [--warmup W] [--workload NAME]
 
 A step is one pass of the whole hot path over one batch: war_verify_step (page
 reservation, embedding, 36 decoder layers with paged GQA verification attention,
@@ -9,15 +9,21 @@ LM head, argmax and greedy acceptance) followed by war_kv_commit.  Each timed st
 discards (accept = -1, the rollback path), so that every step starts from the
 same state.  Inputs are resident in HBM before timing starts.
 
-multi_turn first appends a 2048-token observation to each of 16 cached
-trajectories with war_prefill_append (timed once, reported under "prefill"),
-then times the k = 4 verify step that follows.
+Workloads (all four by default, one after the other, each on its own pool):
+  low_load      8 requests x 32768 cached tokens, k = 8 suffix drafts;
+  high_load     64 requests, lognormal contexts (719,018 tokens), k = 0;
+  high_load_k2  the same contexts, k = 2 sibling drafts, 30% corrupted -- the
+                largest single-GPU workload (121.2 GB per step): the headline;
+  multi_turn    16 trajectories sharing forked prefixes; a 2048-token
+                war_prefill_append each (timed once, under "prefill"), then the
+                k = 4 verify step (HBM bytes count a group's shared prefix once).
 
 Prints ONE JSON line:
-  value     accepted tokens/s = sum_b (accept_b + 1) / step time;
-  roofline  the attention kernel: algorithmic KV bytes per launch / its mean launch
-            time (HIP events on the launch stream, read live) vs 8 TB/s;
-  cpu_baseline the float64 oracle on the host cores, on a bounded sample.
+  value        the headline's accepted tokens/s = sum_b (accept_b + 1) / step time;
+  roofline     its attention kernel: algorithmic KV bytes per launch / its mean
+               launch time (HIP events on the launch stream, read live) vs 8 TB/s;
+  cpu_baseline the float64 oracle on the host cores, on a bounded sample;
+  workloads    the same figures (and a CPU baseline) for every workload.
 """
 from __future__ import annotations
 
@@ -39,8 +45,9 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="low_load",
-                    choices=["low_load", "high_load", "high_load_k2", "multi_turn"])
+    ap.add_argument("--workload", default=None,
+                    choices=["low_load", "high_load", "high_load_k2", "multi_turn"],
+                    help="only this workload (default: all four, headline high_load_k2)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--sweep", action="store_true",
@@ -110,40 +117,48 @@ def measured_traffic(workload: str):
     return rec["workloads"][workload]["traffic_bytes"]
 
 
-def cpu_baseline(cfg, weights, st, kv_seed, sample_layers: int = 8):
-    """Time the oracle on 1 request: embedding + LM head alone, and with
-    `sample_layers` of the 36 layers; the per-request time is extrapolated to
-    all layers."""
-    import numpy as np
+def blas_info():
+    """(vendor, threads) of the BLAS numpy runs on; the threads are set to every
+    core the process may use."""
     import threadpoolctl
-    import torch
+    cores = len(os.sched_getaffinity(0))
+    threadpoolctl.threadpool_limits(limits=cores, user_api="blas")
+    info = [i for i in threadpoolctl.threadpool_info() if i.get("user_api") == "blas"]
+    vendor = info[0].get("internal_api", "unknown") if info else "unknown"
+    threads = max([i.get("num_threads", 1) for i in info] or [1])
+    return cores, vendor, threads
 
+
+def cpu_baseline(cfg, weights, st, kv_get_of, accepted, sample_layers: int = 6):
+    """The float64 oracle on the host cores, on a bounded sample: request 0's
+    embedding + final norm + LM head alone, and with `sample_layers` of the
+    36 layers; the request's time is extrapolated to all layers, and the
+    batch's to B requests (every request runs the same layers)."""
     from oracle.decoder import Weights, forward_block
     from paper_2607_17299_amd import synth
 
+    cores, vendor, threads = blas_info()
     b = 0
     ctx = int(st.ctx_lens[b])
     tokens = [int(st.last_tokens[b])] + list(st.drafts[b])
-
-    def kv_get(l):
-        kv = synth.kv_context(cfg, kv_seed, int(st.seq_ids[b]), l, 0, ctx, "cuda").cpu()
-        a = kv.double().numpy()
-        return a[0], a[1]
+    kv_get = kv_get_of(b, ctx)
 
     def run(n_layers):
-        c = synth.reduced(cfg, n_layers) if n_layers else synth.reduced(cfg, 0)
+        c = synth.reduced(cfg, n_layers)
         W = Weights(c, weights, cache=False)
         t0 = time.perf_counter()
         forward_block(c, W, tokens, ctx, kv_get)
         return time.perf_counter() - t0
 
-    info = threadpoolctl.threadpool_info()
-    threads = max([i.get("num_threads", 1) for i in info] or [1])
     t_head = run(0)
     t_some = run(sample_layers)
     t_req = t_head + (t_some - t_head) * cfg.n_layers / sample_layers
-    return {"t_request_s": t_req, "threads": threads, "t_sample_s": t_head + t_some,
-            "sample_layers": sample_layers}
+    return {"value": round(accepted / (st.B * t_req), 5), "unit": "accepted tokens/s", "cores": cores,
+            "threads": threads, "blas": vendor, "kind": "oracle",
+            "sample": (f"request 0 of {st.B} ({ctx} cached tokens, {len(tokens)} rows): embedding + final "
+                       f"norm + LM head alone, and with {sample_layers} of {cfg.n_layers} layers, timed "
+                       f"({t_head + t_some:.1f} s in all); request time = head + {cfg.n_layers}/"
+                       f"{sample_layers} x (layer part) = {t_req:.1f} s; batch = {st.B} such requests")}
 
 
 def run_sweep(model, cfg, kv_seed, steps, warmup):
@@ -210,13 +225,160 @@ def time_prefill(model, pool, mt, cfg):
             "peak_TFLOPs": 2500.0, "next_tokens": nxt.cpu().numpy()}
 
 
+WORKLOADS = {
+    "low_load": ("low-load rollout verify (cfg2): 36-layer GQA decoder (d 4096, 32q/8kv heads, hd 128, "
+                 "FFN 12288, vocab 151936), 8 requests x 32768 cached tokens, k=8 suffix-drafter drafts"),
+    "high_load": ("high-load rollout decode (cfg3): 36-layer GQA decoder, 64 requests, lognormal contexts "
+                  "(median 8192, sigma 0.8, seed 0), k=0"),
+    "high_load_k2": ("high-load rollout verify (cfg4): 36-layer GQA decoder, 64 requests, lognormal contexts "
+                     "(median 8192, sigma 0.8, seed 0, 719,018 cached tokens), k=2 sibling drafts with 30% of "
+                     "positions corrupted"),
+    "multi_turn": ("multi-turn append (cfg5): 36-layer GQA decoder, 16 trajectories in 4 groups sharing a "
+                   "forked 8192-token prefix, 24576 cached tokens each; war_prefill_append of a 2048-token "
+                   "observation each, then one k=4 verify step"),
+}
+HEADLINE = "high_load_k2"
+
+
+def run_workload(name, model, weights, cfg, args, war, want_cpu, want_variants):
+    """Set up one workload, time its step, profile it; returns its entry and
+    frees its pool."""
+    import numpy as np
+    import torch
+    from paper_2607_17299_amd import harness, synth
+
+    kv_seed = 5
+    t_setup = time.perf_counter()
+    prefill, mt = None, None
+    if name == "low_load":
+        st = harness.low_load_step()
+    elif name == "multi_turn":
+        mt = harness.multi_turn_inputs(vocab=cfg.vocab)
+        pool = harness.multi_turn_pool(cfg, mt, 4, extra_pages=64 + 8 * 16)
+        log("multi_turn: loading cached prefixes (forked) and private contexts")
+        harness.load_multi_turn(pool, cfg, mt, kv_seed)
+        log("multi_turn: prefill-append")
+        prefill = time_prefill(model, pool, mt, cfg)
+        st = harness.multi_turn_step(mt, prefill.pop("next_tokens"), 4)
+    else:
+        st = harness.high_load_step(k=0)
+    log(f"workload {name}: B={st.B} k={st.k_max} sum ctx={int(st.ctx_lens.sum())}")
+    if name != "multi_turn":
+        # spare pages for the steps in flight: the host never waits for the free count
+        k_res = 2 if name == "high_load_k2" else st.k_max
+        pool = harness.make_pool(cfg, st.ctx_lens, max(k_res, 2) + 8,
+                                 extra_pages=64 + 8 * st.B * harness.cdiv(k_res + 1, cfg.page_size))
+        log(f"{name}: loading cached contexts")
+        harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, kv_seed)
+    if name == "high_load_k2":
+        cont = harness.teacher_continuation(model, pool, st, 2)
+        drafts = harness.corrupt(cont, 0.3, seed=4, vocab=cfg.vocab)
+        st = harness.Step(st.seq_ids, st.ctx_lens, st.last_tokens, drafts, 2)
+    ds = harness.DeviceStep(st)
+    log(f"{name}: setup {time.perf_counter() - t_setup:.1f}s; warmup {args.warmup}")
+    for _ in range(args.warmup):
+        ds.verify(model, pool)
+        ds.commit(pool, discard=True)
+    torch.cuda.synchronize()
+    waits0 = pool.waits()
+    ms = timed_steps(ds, model, pool, args.steps)
+    waits = pool.waits() - waits0
+    acc = ds.accept.cpu().numpy()
+    accepted = int((acc + 1).sum())
+    log(f"{name}: {ms:.3f} ms/step, accept {acc.tolist()}")
+    dist = step_distribution(ds, model, pool, args.steps)
+    prof = kernel_profile(ds, model, pool, war)
+    attn = prof.get("attention", {"calls": 0, "ms": 0.0})
+    per_launch_ms = attn["ms"] / max(attn["calls"], 1)
+    kv_bytes = harness.step_kv_bytes(cfg, st, mt)
+    attn_gbps = kv_bytes / (per_launch_ms * 1e-3) / 1e9
+    total_bytes = harness.step_bytes(cfg, st, shared_prefix=mt)
+    step_gbps = total_bytes / (ms * 1e-3) / 1e9
+    entry = {
+        "workload": WORKLOADS[name], "batch": st.B, "k": st.k_max, "rows": st.rows(),
+        "sum_ctx": int(st.ctx_lens.sum()), "ms_per_step": round(ms, 4),
+        "accepted_tokens_per_s": round(accepted / (ms / 1e3), 2),
+        "verified_positions_per_s": round(st.rows() / (ms / 1e3), 1),
+        "accept_lens": acc.tolist(),
+        "hbm": {"step_bytes": total_bytes, "achieved_GBps": round(step_gbps, 1),
+                "frac_of_peak": round(step_gbps / HBM_PEAK_GBPS, 4),
+                "bytes": ("weights + every visible key and value (a group's shared prefix once) + the new "
+                          "rows' KV" if mt else "weights + every visible key and value + the new rows' KV")},
+        "roofline": {"kernel": "attention (k_attn)", "bound": "hbm", "achieved": round(attn_gbps, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
+                     "bytes_per_launch": kv_bytes, "mean_launch_ms": round(per_launch_ms, 5),
+                     "traffic": measured_traffic(name)},
+        "step_ms_events": dist, "host_waits_for_free_count": waits, "kernels_ms_per_step": prof,
+    }
+    if prefill is not None:
+        entry["prefill"] = prefill
+    variants = {}
+    if want_variants and name in ("low_load", "multi_turn"):
+        # the same requests, drafting from a sibling rollout that produced the
+        # target's own continuation (GRPO siblings): drafts are accepted
+        cont = harness.teacher_continuation(model, pool, st, st.k_max + 1)
+        st2 = (harness.low_load_step(siblings=cont) if name == "low_load"
+               else harness.multi_turn_step(mt, st.last_tokens, st.k_max, siblings=cont))
+        variants["sibling_drafts"] = time_variant(harness.DeviceStep(st2), model, pool, args.steps)
+        if name == "low_load":
+            # three siblings per request that leave the target's continuation at
+            # different tokens: a k-token chain against a k-node tree
+            sets = harness.diverging_siblings(cont, 3, cfg.vocab)
+            for vname, tree in (("diverging_siblings_chain", False), ("diverging_siblings_tree", True)):
+                ds3 = harness.DeviceStep(harness.low_load_step(sibling_sets=sets, tree=tree))
+                variants[vname] = time_variant(ds3, model, pool, args.steps)
+            # sampled verification in the paper's setting (temperature 1, top-k
+            # 200), same requests and drafts; uniforms drawn once on the device
+            g = torch.Generator(device="cuda")
+            g.manual_seed(7)
+            uni = torch.rand((st.B * (st.k_max + 1), 2), generator=g, device="cuda", dtype=torch.float32)
+            variants["sampled_T1_top200"] = time_variant(ds, model, pool, args.steps, uniforms=uni)
+            entry["drafter_host"] = harness.time_low_load_drafter()
+    if variants:
+        entry["variants"] = variants
+    if want_cpu:
+        log(f"{name}: timing the oracle on the host")
+        if mt is not None:
+            kv_get_of = lambda b, ctx: (lambda l: tuple(pool.gather_kv(int(st.seq_ids[b]), ctx, l)
+                                                        .cpu().double().numpy()))
+        else:
+            kv_get_of = lambda b, ctx: (lambda l: tuple(synth.kv_context(cfg, kv_seed, int(st.seq_ids[b]), l, 0,
+                                                                         ctx, "cuda").cpu().double().numpy()))
+        entry["cpu_baseline"] = cpu_baseline(cfg, weights, st, kv_get_of, accepted)
+    pool.close()
+    del pool
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return entry
+
+
+def time_variant(ds, model, pool, steps, uniforms=None):
+    import torch
+    if uniforms is not None:
+        run = lambda: ds.verify_sampled(model, pool, uniforms)
+    else:
+        run = lambda: ds.run(model, pool)
+    for _ in range(2):
+        run()
+        ds.commit(pool, discard=True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        run()
+        ds.commit(pool, discard=True)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / steps
+    acc = ds.accept.cpu().numpy()
+    return {"ms_per_step": round(ms, 4), "accepted_tokens_per_s": round(float((acc + 1).sum() / (ms / 1e3)), 1),
+            "accept_lens": acc.tolist()}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "this build runs on one GPU; --gpus must be 1",
                           "n_gpus": args.gpus}))
         sys.exit(2)
-    import numpy as np
     import torch
 
     if args.copy_probe:
@@ -238,155 +400,31 @@ def main():
     from paper_2607_17299_amd import harness, synth, war
 
     cfg = synth.LARGE
-    t_setup = time.perf_counter()
     log("generating weights on the GPU")
     weights = harness.large_weights(cfg)
     model = war.Model(cfg, weights, max_rows=1152 if args.sweep else 1024)
-    kv_seed = 5
     if args.sweep:
-        print(json.dumps(run_sweep(model, cfg, kv_seed, min(args.steps, 10), args.warmup)), flush=True)
+        print(json.dumps(run_sweep(model, cfg, 5, min(args.steps, 10), args.warmup)), flush=True)
         return
-    prefill = None
-    if args.workload == "low_load":
-        st = harness.low_load_step()
-        desc = ("low-load rollout verify: 36-layer GQA decoder (d 4096, 32q/8kv heads, hd 128, FFN 12288, "
-                "vocab 151936), 8 requests x 32768 cached tokens, k=8 suffix-drafter drafts")
-    elif args.workload == "multi_turn":
-        mt = harness.multi_turn_inputs(vocab=cfg.vocab)
-        desc = ("multi-turn append: 36-layer GQA decoder, 16 trajectories in 4 groups sharing a forked "
-                "8192-token prefix, 24576 cached tokens each; war_prefill_append of a 2048-token "
-                "observation each, then one k=4 verify step (suffix drafts over the group's siblings)")
-        pool = harness.multi_turn_pool(cfg, mt, 4)
-        log("loading cached prefixes (forked) and private contexts")
-        harness.load_multi_turn(pool, cfg, mt, kv_seed)
-        log("prefill-append")
-        prefill = time_prefill(model, pool, mt, cfg)
-        st = harness.multi_turn_step(mt, prefill.pop("next_tokens"), 4)
-    else:
-        k = 2 if args.workload == "high_load_k2" else 0
-        st = harness.high_load_step(k=0)
-        desc = ("high-load rollout %s: 36-layer GQA decoder, 64 requests, lognormal contexts "
-                "(median 8192, sigma 0.8, seed 0)" % ("verify k=2 (sibling drafts, 30%% corrupted)" if k else "decode k=0"))
-    log(f"workload {args.workload}: B={st.B} k={st.k_max} sum ctx={int(st.ctx_lens.sum())}")
-    if args.workload != "multi_turn":
-        pool = harness.make_pool(cfg, st.ctx_lens, max(st.k_max, 2) + 8)
-        log("loading cached contexts")
-        harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, kv_seed)
-    if args.workload == "high_load_k2":
-        cont = harness.teacher_continuation(model, pool, st, 2)
-        drafts = harness.corrupt(cont, 0.3, seed=4, vocab=cfg.vocab)
-        st = harness.Step(st.seq_ids, st.ctx_lens, st.last_tokens, drafts, 2)
-    ds = harness.DeviceStep(st)
-    log(f"setup {time.perf_counter() - t_setup:.1f}s; warmup {args.warmup}")
-    for _ in range(args.warmup):
-        ds.verify(model, pool)
-        ds.commit(pool, discard=True)
-    torch.cuda.synchronize()
-    ms = timed_steps(ds, model, pool, args.steps)
-    acc = ds.accept.cpu().numpy()
-    accepted = int((acc + 1).sum())
-    value = accepted / (ms / 1e3)
-    log(f"{ms:.3f} ms/step, accept {acc.tolist()}")
-
-    dist = step_distribution(ds, model, pool, args.steps)
-    prof = kernel_profile(ds, model, pool, war)
-    attn = prof.get("attention", {"calls": 0, "ms": 0.0})
-    per_launch_ms = attn["ms"] / max(attn["calls"], 1)
-    kv_bytes = harness.step_kv_bytes(cfg, st)
-    attn_gbps = kv_bytes / (per_launch_ms * 1e-3) / 1e9
-    total_bytes = harness.step_bytes(cfg, st)
-    step_gbps = total_bytes / (ms * 1e-3) / 1e9
-    traffic = measured_traffic(args.workload)
-
-    variants = {}
-    if args.workload in ("low_load", "multi_turn") and not args.no_variants:
-        # the same requests, drafting from a sibling rollout that produced the
-        # target's own continuation (GRPO siblings): drafts are accepted
-        cont = harness.teacher_continuation(model, pool, st, st.k_max + 1)
-        st2 = (harness.low_load_step(siblings=cont) if args.workload == "low_load"
-               else harness.multi_turn_step(mt, st.last_tokens, st.k_max, siblings=cont))
-        ds2 = harness.DeviceStep(st2)
-        for _ in range(2):
-            ds2.verify(model, pool)
-            ds2.commit(pool, discard=True)
-        ms2 = timed_steps(ds2, model, pool, args.steps)
-        acc2 = ds2.accept.cpu().numpy()
-        variants["sibling_drafts"] = {"ms_per_step": round(ms2, 4),
-                                      "accepted_tokens_per_s": round(float((acc2 + 1).sum() / (ms2 / 1e3)), 1),
-                                      "accept_lens": acc2.tolist()}
-        if args.workload == "low_load":
-            # three siblings per request that leave the target's continuation at
-            # different tokens: a k-token chain against a k-node tree
-            sets = harness.diverging_siblings(cont, 3, cfg.vocab)
-            for name, tree in (("diverging_siblings_chain", False), ("diverging_siblings_tree", True)):
-                ds3 = harness.DeviceStep(harness.low_load_step(sibling_sets=sets, tree=tree))
-                for _ in range(2):
-                    ds3.run(model, pool)
-                    ds3.commit(pool, discard=True)
-                ms3 = timed_steps(ds3, model, pool, args.steps)
-                acc3 = ds3.accept.cpu().numpy()
-                variants[name] = {"ms_per_step": round(ms3, 4),
-                                  "accepted_tokens_per_s": round(float((acc3 + 1).sum() / (ms3 / 1e3)), 1),
-                                  "accept_lens": acc3.tolist()}
-
-    if not args.no_variants:
-        # sampled verification in the paper's setting (temperature 1, top-k 200),
-        # same requests and drafts; uniforms drawn once on the device
-        g = torch.Generator(device="cuda")
-        g.manual_seed(7)
-        uni = torch.rand((st.B * (st.k_max + 1), 2), generator=g, device="cuda", dtype=torch.float32)
-        for _ in range(2):
-            ds.verify_sampled(model, pool, uni)
-            ds.commit(pool, discard=True)
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        for _ in range(args.steps):
-            ds.verify_sampled(model, pool, uni)
-            ds.commit(pool, discard=True)
-        torch.cuda.synchronize()
-        ms3 = (time.perf_counter() - t0) * 1e3 / args.steps
-        acc3 = ds.accept.cpu().numpy()
-        variants["sampled_T1_top200"] = {"ms_per_step": round(ms3, 4),
-                                         "accepted_tokens_per_s": round(float((acc3 + 1).sum() / (ms3 / 1e3)), 1),
-                                         "accept_lens": acc3.tolist()}
-
-    drafter = None
-    if args.workload == "low_load":
-        drafter = harness.time_low_load_drafter()
-
-    cpu = None
-    if not args.no_cpu_baseline:
-        log("timing the oracle on the host")
-        c = cpu_baseline(cfg, weights, st, kv_seed)
-        # oracle throughput: the sampled request's accepted tokens over B sequential requests
-        cpu = {"value": round(accepted / (st.B * c["t_request_s"]), 4), "unit": "accepted tokens/s",
-               "cores": c["threads"], "kind": "oracle",
-               "sample": (f"request 0 of {st.B}: embedding + final norm + LM head alone, and with "
-                          f"{c['sample_layers']} of 36 layers, timed ({c['t_sample_s']:.1f}s in all); "
-                          f"per-request time = head + 36/{c['sample_layers']} x (layer part) "
-                          f"= {c['t_request_s']:.1f}s; every request costs the same")}
-
+    names = [args.workload] if args.workload else ["low_load", "high_load", "high_load_k2", "multi_turn"]
+    head = args.workload or HEADLINE
+    entries = {}
+    for name in names:
+        entries[name] = run_workload(name, model, weights, cfg, args, war,
+                                     want_cpu=not args.no_cpu_baseline, want_variants=not args.no_variants)
+    e = entries[head]
     out = {
-        "metric": METRIC, "value": round(value, 2), "unit": "accepted tokens/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+        "metric": METRIC, "value": e["accepted_tokens_per_s"], "unit": "accepted tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": e["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded random-init weights, seeded cached KV, motif-built token streams)",
-        "config": {"workload": desc, "batch": st.B, "k": st.k_max, "rows": st.rows(),
-                   "sum_ctx": int(st.ctx_lens.sum()), "parallelism": "single GPU"},
-        "hbm": {"step_bytes": total_bytes, "achieved_GBps": round(step_gbps, 1),
-                "frac_of_peak": round(step_gbps / HBM_PEAK_GBPS, 4)},
-        "verified_positions_per_s": round(st.rows() / (ms / 1e3), 1),
-        "step_ms_events": dist,
-        "drafter_host": drafter,
-        "accept_lens": acc.tolist(),
-        "roofline": {"kernel": "attention (k_attn)", "bound": "hbm", "achieved": round(attn_gbps, 1),
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": round(attn_gbps / HBM_PEAK_GBPS, 4),
-                     "bytes_per_launch": kv_bytes, "mean_launch_ms": round(per_launch_ms, 5),
-                     "traffic": traffic},
-        "kernels_ms_per_step": prof,
-        "prefill": prefill,
-        "variants": variants,
-        "cpu_baseline": cpu,
+        "config": {"workload": e["workload"], "batch": e["batch"], "k": e["k"], "rows": e["rows"],
+                   "sum_ctx": e["sum_ctx"], "parallelism": "single GPU"},
+        "hbm": e["hbm"], "roofline": e["roofline"], "cpu_baseline": e.get("cpu_baseline"),
+        "verified_positions_per_s": e["verified_positions_per_s"], "step_ms_events": e["step_ms_events"],
+        "kernels_ms_per_step": e["kernels_ms_per_step"],
+        "workloads": {n: {k: v for k, v in x.items() if k != "kernels_ms_per_step" or n != head}
+                      for n, x in entries.items()},
     }
     print(json.dumps(out), flush=True)
 

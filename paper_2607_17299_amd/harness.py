@@ -353,18 +353,25 @@ def multi_turn_step(mt: MultiTurn, next_tokens, k: int = 4,
     return Step(mt.seq_ids, np.full(mt.n, mt.cached + mt.n_new, np.int32), nxt, drafts, k)
 
 
-def step_kv_bytes(cfg: synth.ModelConfig, st: Step) -> int:
-    """KV bytes one layer's attention must read: every visible key and value."""
+def step_kv_bytes(cfg: synth.ModelConfig, st: Step, shared_prefix: Optional[MultiTurn] = None) -> int:
+    """KV bytes one layer's attention must read: every visible key and value.
+    With ``shared_prefix`` (forked siblings) a group's common prefix counts
+    once: the unique bytes."""
     per_tok = 2 * cfg.n_kv_heads * cfg.head_dim * 2
-    return int(sum(int(c) + len(d) + 1 for c, d in zip(st.ctx_lens, st.drafts))) * per_tok
+    toks = int(sum(int(c) + len(d) + 1 for c, d in zip(st.ctx_lens, st.drafts)))
+    if shared_prefix is not None:
+        mt = shared_prefix
+        toks -= (mt.n - mt.groups) * mt.prefix
+    return toks * per_tok
 
 
-def step_bytes(cfg: synth.ModelConfig, st: Step, logits: bool = False) -> int:
+def step_bytes(cfg: synth.ModelConfig, st: Step, logits: bool = False,
+               shared_prefix: Optional[MultiTurn] = None) -> int:
     """Algorithmic HBM bytes of one verify step: streamed weights, KV read and
     KV written (every layer), logits if written."""
     kv_tok = cfg.kv_bytes_per_token()
     T = st.rows()
-    b = cfg.streamed_weight_bytes() + cfg.n_layers * step_kv_bytes(cfg, st) + T * kv_tok
+    b = cfg.streamed_weight_bytes() + cfg.n_layers * step_kv_bytes(cfg, st, shared_prefix) + T * kv_tok
     if logits:
         b += 4 * T * cfg.vocab
     return b
