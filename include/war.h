@@ -242,6 +242,29 @@ war_status war_verify_step_tree(war_model* m, war_kv_pool* p, int32_t B, const i
                                 const int32_t* draft_lens, int32_t k_max, int32_t* accept_lens,
                                 int32_t* next_tokens, int32_t* accept_path, float* logits, void* stream);
 
+/* war_verify_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc).
+ * Same arguments, pool protocol and results as war_verify_step (greedy chain
+ * drafts); the step's workspace (activations, split-K partials, attention
+ * work list and partials, counters) is laid over a static device array of
+ * 64 MiB that the library holds on each GPU it runs on until the process
+ * ends, instead of the model's own workspace.  This call allocates nothing:
+ * no hipMalloc, hipFree or allocating library routine, and no host buffers.
+ * It returns WAR_ERR_UNSUPPORTED (enqueuing nothing) when the step does not
+ * fit: the rows B*(k_max+1) with their partials, plus the attention items of
+ * B requests of max_pages_per_seq pages (longer attention chunks are taken
+ * first to fit).  When the host's lower bound on free pages does not cover
+ * B*ceil((k_max+1)/16) pages it reads the exact count (one stream
+ * synchronisation) and returns WAR_ERR_OUT_OF_PAGES if that does not cover
+ * it either.  Every call on one GPU shares that GPU's array: calls that
+ * overlap on one GPU (other streams, other threads) race; the array keeps the
+ * last call's contents, and the step clears what must start at zero. */
+war_status war_verify_step_noalloc(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                                   const int32_t* ctx_lens, const int32_t* last_tokens,
+                                   const int32_t* draft_tokens, const int32_t* draft_lens, int32_t k_max,
+                                   int32_t* accept_lens, int32_t* next_tokens, float* logits,
+                                   void* stream);
+
 /* Commit the pending verify step.
  *   accept_lens device int32 [B]; -1 discards the step.  Values are clamped
  *               to [-1, reserved capacity].

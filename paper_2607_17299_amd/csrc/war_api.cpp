@@ -6,6 +6,7 @@
 #include <algorithm>
 #include <cmath>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <unordered_set>
 #include <vector>
@@ -188,6 +189,38 @@ size_t ws_layout(const ModelDims& md, int R, int64_t items, int rb, int64_t p_el
   v.po = reinterpret_cast<float*>(take(pr * md.hd * 4));
   if (w) *w = v;
   return off;
+}
+
+// ---- static device scratch (war_verify_step_noalloc)
+// A fixed array in device memory that every GPU the library runs on holds
+// until the process ends.  Host code never uses its name as an address: the
+// name is a host-side stand-in.  scratch_address() asks the runtime for the
+// current device's copy once (hipGetSymbolAddress) and keeps it per device.
+constexpr size_t kScratchBytes = size_t(64) << 20;
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+}  // namespace
+
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+
+// The current device's copy of `scratch` (out may be null: set-up only).
+war_status scratch_address(void** out) {
+  int dev = 0;
+  HIPCHK(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return fail(WAR_ERR_UNSUPPORTED, "device index beyond the scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* ptr = nullptr;
+    HIPCHK(hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)));
+    if (!ptr) return fail(WAR_ERR_HIP, "hipGetSymbolAddress returned no address for the scratch array");
+    g_scratch_ptr[dev] = ptr;
+  }
+  if (out) *out = g_scratch_ptr[dev];
+  return WAR_OK;
 }
 
 }  // namespace
@@ -637,6 +670,12 @@ war_status war_model_create(const war_model_config* cfg, const void* const* weig
     war_model_destroy(m);
     return fail(ws, msg);
   }
+  // this device's copy of the static scratch array, for war_verify_step_noalloc
+  if (war_status ss = scratch_address(nullptr); ss != WAR_OK) {
+    const std::string msg = g_err;
+    war_model_destroy(m);
+    return fail(ss, msg);
+  }
   *out = m;
   return WAR_OK;
 }
@@ -895,7 +934,7 @@ war_status verify_impl(war_model* m, war_kv_pool* p, int32_t B, const int32_t* s
     }
     if (bytes > fixed->bytes)
       return fail(WAR_ERR_UNSUPPORTED, "the step's workspace (" + std::to_string(bytes) +
-                                           " bytes) exceeds the fixed region (" +
+                                           " bytes) exceeds the static scratch (" +
                                            std::to_string(fixed->bytes) + " bytes)");
     ws_layout(m->md, R, max_items, RB, pel, fixed->base, &wsv);
   } else {
@@ -1050,6 +1089,23 @@ war_status war_verify_step_tree(war_model* m, war_kv_pool* p, int32_t B, const i
   CHECK(k_max == 0 || draft_parents, "draft_parents required when k_max > 0");
   return verify_impl(m, p, B, seq_ids, ctx_lens, last_tokens, draft_tokens, draft_lens, k_max, accept_lens,
                      next_tokens, logits, stream, SampleParams{}, draft_parents, accept_path);
+}
+
+war_status war_verify_step_noalloc(war_model* m, war_kv_pool* p, int32_t B, const int32_t* seq_ids,
+                                   const int32_t* ctx_lens, const int32_t* last_tokens,
+                                   const int32_t* draft_tokens, const int32_t* draft_lens, int32_t k_max,
+                                   int32_t* accept_lens, int32_t* next_tokens, float* logits, void* stream) {
+  CHECK(m, "null model");
+  void* base = nullptr;
+  war_status s = scratch_address(&base);
+  if (s != WAR_OK) return s;
+  const StaticWs fixed{static_cast<char*>(base), kScratchBytes};
+  const bool prof = m->prof.on;  // the profiler creates events: off for this call
+  m->prof.on = false;
+  s = verify_impl(m, p, B, seq_ids, ctx_lens, last_tokens, draft_tokens, draft_lens, k_max, accept_lens,
+                  next_tokens, logits, stream, SampleParams{}, nullptr, nullptr, &fixed);
+  m->prof.on = prof;
+  return s;
 }
 
 war_status war_kv_commit(war_kv_pool* p, int32_t B, const int32_t* seq_ids, int32_t* ctx_lens,

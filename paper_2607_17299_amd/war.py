@@ -26,6 +26,7 @@ _ERRORS = {-1: "WAR_ERR_INVALID_ARG", -2: "WAR_ERR_OUT_OF_PAGES", -3: "WAR_ERR_H
 EXPORTS = ["war_weight_count", "war_model_create", "war_model_destroy", "war_kv_pool_create",
            "war_kv_pool_destroy", "war_kv_alloc", "war_kv_fork", "war_kv_free", "war_kv_load",
            "war_prefill_append", "war_verify_step", "war_verify_step_sampled", "war_verify_step_tree",
+           "war_verify_step_noalloc",
            "war_kv_commit", "war_pool_state",
            "war_last_error", "war_debug_mfma16", "war_debug_workspace", "war_debug_sample",
            "war_debug_pool_waits", "war_profile", "war_profile_read"]
@@ -64,6 +65,7 @@ def load_library(path: str = LIB_PATH) -> C.CDLL:
         "war_verify_step_sampled": (i32, [vp, vp, i32, vp, vp, vp, vp, vp, i32, vp, C.c_float, i32,
                                           vp, vp, vp, vp]),
         "war_verify_step_tree": (i32, [vp, vp, i32, vp, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp, vp]),
+        "war_verify_step_noalloc": (i32, [vp, vp, i32, vp, vp, vp, vp, vp, i32, vp, vp, vp, vp]),
         "war_kv_commit": (i32, [vp, i32, vp, vp, vp, vp]),
         "war_pool_state": (i32, [vp, pi32, pi32, pi32, pi32, pi32, vp]),
         "war_last_error": (C.c_char_p, []),
@@ -229,6 +231,17 @@ def verify_step(model: Model, pool: Pool, seq_ids: torch.Tensor, ctx_lens: torch
     _check(lib().war_verify_step(model.handle, pool.handle, B, _ptr(seq_ids), _ptr(ctx_lens),
                                  _ptr(last_tokens), _ptr(draft_tokens), _ptr(draft_lens), k_max,
                                  _ptr(accept_lens), _ptr(next_tokens), _ptr(logits), _stream(stream)))
+
+
+def verify_step_noalloc(model: Model, pool: Pool, seq_ids: torch.Tensor, ctx_lens: torch.Tensor,
+                        last_tokens: torch.Tensor, draft_tokens: Optional[torch.Tensor],
+                        draft_lens: Optional[torch.Tensor], k_max: int, accept_lens: torch.Tensor,
+                        next_tokens: torch.Tensor, logits: Optional[torch.Tensor] = None, stream=None) -> None:
+    """war_verify_step over the library's static device scratch (allocates nothing)."""
+    B = seq_ids.numel()
+    _check(lib().war_verify_step_noalloc(model.handle, pool.handle, B, _ptr(seq_ids), _ptr(ctx_lens),
+                                         _ptr(last_tokens), _ptr(draft_tokens), _ptr(draft_lens), k_max,
+                                         _ptr(accept_lens), _ptr(next_tokens), _ptr(logits), _stream(stream)))
 
 
 def verify_step_sampled(model: Model, pool: Pool, seq_ids: torch.Tensor, ctx_lens: torch.Tensor,
