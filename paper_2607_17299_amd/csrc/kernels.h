@@ -89,8 +89,9 @@ void launch_kv_load(const PoolDev& p, const KvGeom& g, int seq, int layer, int p
 void launch_add_ctx(int n, int32_t* ctx, const int32_t* add, hipStream_t st);
 
 // GEMM (gemm.hip)
-int gemm_mt(int M);  // 16-row tiles per m-block for M rows
-int gemm_mw(int M);  // m-blocks per workgroup (non-argmax epilogues)
+int gemm_mt(int M);             // 16-row tiles per m-block for M rows
+int gemm_mw(int M);             // m-blocks per workgroup
+int gemm_mblock_groups(int M);  // workgroups per 128-column block and split
 void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st);
 // W [N][K] row-major -> dst in MFMA fragment order; N % 16 == 0, K % 64 == 0
 // Repack [N][K] weights (N % 128 == 0) into the GEMM's grouped fragment order;

@@ -358,9 +358,7 @@ struct Timed {
 // write and to add up afterwards; below ~192 workgroups too few CUs stream W
 // (measured on the 4096- and 6144-wide projections: 192-256 is the optimum).
 Split pick_split(int M, int N, int K, int64_t cap_elems) {
-  const int mt = gemm_mt(M);
-  const int mblocks = cdiv_i(M, mt * 16 * gemm_mw(M));  // workgroups per n-block and split
-  const int base = (N / 128) * mblocks;
+  const int base = (N / 128) * gemm_mblock_groups(M);  // workgroups per split
   for (int s = 1; s <= 64; ++s) {
     if (K % (s * 64)) continue;
     if ((int64_t)base * s >= 192 && (int64_t)s * M * N <= cap_elems) return {s, K / s};
