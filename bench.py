@@ -254,7 +254,7 @@ def run_workload(name, model, weights, cfg, args, war, want_cpu, want_variants):
         st = harness.low_load_step()
     elif name == "multi_turn":
         mt = harness.multi_turn_inputs(vocab=cfg.vocab)
-        pool = harness.multi_turn_pool(cfg, mt, 4, extra_pages=64 + 8 * 16)
+        pool = harness.multi_turn_pool(cfg, mt, 4, extra_pages=64 + max(40, args.steps + 8) * 16)
         log("multi_turn: loading cached prefixes (forked) and private contexts")
         harness.load_multi_turn(pool, cfg, mt, kv_seed)
         log("multi_turn: prefill-append")
@@ -262,18 +262,23 @@ def run_workload(name, model, weights, cfg, args, war, want_cpu, want_variants):
         st = harness.multi_turn_step(mt, prefill.pop("next_tokens"), 4)
     else:
         st = harness.high_load_step(k=0)
-    log(f"workload {name}: B={st.B} k={st.k_max} sum ctx={int(st.ctx_lens.sum())}")
     if name != "multi_turn":
-        # spare pages for the steps in flight: the host never waits for the free count
+        # Spare pages for the steps in flight.  The host may run every timed
+        # step ahead of the device; each verify step lowers the host's bound on
+        # the free count by B * ceil((k+1)/page) until the commit report of an
+        # earlier step raises it again, so this many spare pages mean the host
+        # never waits for the exact count.
         k_res = 2 if name == "high_load_k2" else st.k_max
+        in_flight = max(40, args.steps + 8)
         pool = harness.make_pool(cfg, st.ctx_lens, max(k_res, 2) + 8,
-                                 extra_pages=64 + 8 * st.B * harness.cdiv(k_res + 1, cfg.page_size))
+                                 extra_pages=64 + in_flight * st.B * harness.cdiv(k_res + 1, cfg.page_size))
         log(f"{name}: loading cached contexts")
         harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, kv_seed)
     if name == "high_load_k2":
         cont = harness.teacher_continuation(model, pool, st, 2)
         drafts = harness.corrupt(cont, 0.3, seed=4, vocab=cfg.vocab)
         st = harness.Step(st.seq_ids, st.ctx_lens, st.last_tokens, drafts, 2)
+    log(f"workload {name}: B={st.B} k={st.k_max} sum ctx={int(st.ctx_lens.sum())}")
     ds = harness.DeviceStep(st)
     log(f"{name}: setup {time.perf_counter() - t_setup:.1f}s; warmup {args.warmup}")
     for _ in range(args.warmup):
