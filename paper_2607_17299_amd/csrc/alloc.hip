@@ -260,7 +260,21 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
   int n_units;
   const int noff = block_excl_scan(n_mine, sh, &n_units);
   if (t < a.B) s_noff[t] = noff;
+  // A batch without forked siblings takes every request's whole chunks first,
+  // in request order, then the partial last chunks, longest first: the
+  // persistent grid then ends on its shortest units (s_mis is free by now and
+  // holds each request's partial length).
+  __shared__ int s_grp;
+  if (t == 0) s_grp = 0;
   __syncthreads();
+  if (t < a.B && g > 1) s_grp = 1;  // every writer stores 1
+  const int len = (t < a.B && nch > 0) ? ctx + dl + 1 : 0;
+  const int n_whole = len / chunk, rem = len % chunk;
+  if (t < a.B) s_mis[t] = rem;
+  __syncthreads();
+  const bool lpt = s_grp == 0;
+  int n_whole_all;
+  const int woff = block_excl_scan(lpt ? n_whole : 0, sh, &n_whole_all);
   // Work order.  A group without shared units whose members have equal chunk
   // counts gets its items interleaved chunk-major (the members read a shared
   // chunk at the same time, so later readers find it in cache); otherwise
@@ -273,7 +287,17 @@ __global__ void __launch_bounds__(kBT) k_verify_setup(PoolDev p, VerifySetupArgs
       m.udesc[2 * o] = make_int4(ioff + c, t, c, (dl + 1) << 16);  // first token 0, dl + 1 rows' tokens
       m.udesc[2 * o + 1] = make_int4(wc, s, ctx, t * kp1);
     };
-    if (nsc == 0 && g > 1 && regular) {
+    if (lpt) {
+      for (int c = 0; c < n_whole; ++c) put(woff + c, c);
+      if (rem > 0) {
+        int rank = 0;  // partial chunks longer than this one, ties by request
+        for (int q = 0; q < a.B; ++q) {
+          const int rq = s_mis[q];
+          rank += rq > rem || (rq == rem && q < t);
+        }
+        put(n_whole_all + rank, n_whole);
+      }
+    } else if (nsc == 0 && g > 1 && regular) {
       for (int c = 0; c < nch; ++c) put(s_noff[L] + c * g + j, c);
     } else {
       int o = noff;
