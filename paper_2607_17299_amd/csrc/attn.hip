@@ -437,6 +437,270 @@ k_attn(AttnArgs a) {
   }
 }
 
+// One unit's rows and keys, decoded from its work-order descriptor (the fields
+// k_attn reads inline; prefill units are never shared-prefix units).
+struct UnitRows {
+  int item, b, chunk, t0, nt, seq, pos0, row0, nrows, last_pos;
+  __device__ void decode(const AttnArgs& a, int it) {
+    const int4 u0 = a.meta.udesc[2 * (it / a.n_kv_heads)], u1 = a.meta.udesc[2 * (it / a.n_kv_heads) + 1];
+    item = u0.x;
+    b = u0.y;
+    chunk = u0.z;
+    t0 = u0.w & 0xffff;
+    nt = u0.w >> 16;
+    seq = u1.y;
+    pos0 = u1.z;
+    row0 = u1.w;
+    nrows = nt * a.G;
+    last_pos = pos0 + t0 + nt - 1;
+  }
+  // row r -> (query row, query head) and its partial row; false if r is not live
+  __device__ bool src(const AttnArgs& a, int kvh, int r, int& qrow, int& h, int64_t& prow) const {
+    if (r >= nrows) return false;
+    qrow = a.meta.req_row0[b] + t0 + r / a.G;
+    h = kvh * a.G + r % a.G;
+    prow = ((int64_t)item * a.n_kv_heads + kvh) * a.prb + r;
+    return true;
+  }
+};
+
+// Prefill attention over row blocks of NW * 32 rows (a causal run of a
+// sequence's new tokens; G query heads per token).  Wave w owns rows
+// [32w, 32w + 32): two 16-row tiles, queries in registers.  The NW waves share
+// every 32-key block, which all threads stage through LDS (two buffers, with
+// the next two blocks in flight in registers; K rows and V^T rows padded
+// against bank conflicts; V^T columns past the sequence end zeroed), so a key
+// block is read from memory once per NW * 32 rows instead of once per 48 rows
+// as in k_attn.  Per block and wave: S^T = K Q^T
+// for both row tiles (each K fragment read once from LDS), the online softmax
+// of k_attn, and O^T += V^T P^T with P as bf16 hi + lo (each V^T fragment read
+// once for both tiles).  Work units, partials and the merge are k_attn's.
+template <int NW, int HD>
+__global__ void __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2, 2)))
+k_attn_rows(AttnArgs a) {
+  constexpr int KSUB = HD / 32;  // MFMA k-steps over the head dim
+  constexpr int NDT = HD / 16;   // 16-dim output tiles
+  constexpr int NRW = 2;         // 16-row tiles per wave
+  constexpr int NT = NW * 64;    // threads
+  constexpr int KST = HD + 8;    // LDS row stride (bf16) of K [32 keys][HD]
+  constexpr int VST = 32 + 8;    // LDS row stride (bf16) of V^T [HD][32 keys]
+  __shared__ __attribute__((aligned(16))) bf16_t s_k[2][32 * KST];
+  __shared__ __attribute__((aligned(16))) bf16_t s_v[2][HD * VST];
+  const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int total = a.meta.n_items[1] * a.n_kv_heads;
+  const int CH = a.meta.n_items[3];
+  const int P = a.kv.page_size;
+  // key row of this lane in S^T tile t of a block: (ln/4)*8 + ln%4 + 4t
+  const int kk0 = (ln >> 2) * 8 + (ln & 3);
+
+  const int NC = min(8, (int)gridDim.x);
+  const int cls = blockIdx.x % NC;
+  __shared__ int s_it;
+  if (tid == 0) s_it = atomicAdd(&a.unit_ctr[cls], 1) * NC + cls;
+  __syncthreads();
+  for (;;) {
+    const int it = s_it;
+    if (it >= total) break;
+    const int kvh = it % a.n_kv_heads;
+    UnitRows u;
+    u.decode(a, it);
+    const int S = u.last_pos + 1;
+    const int qpos0 = u.pos0 + u.t0;  // the first row's position
+    const int kbeg = u.chunk * CH, kend = min(S, kbeg + CH);
+    const int nb = kend > kbeg ? (kend - kbeg + 31) / 32 : 0;
+    // blocks before nfull lie at or below every row's position
+    const int nfull = qpos0 - 31 - kbeg < 0 ? 0 : min(nb, (qpos0 - 31 - kbeg) / 32 + 1);
+    const int32_t* trow = a.table + (int64_t)u.seq * a.max_pages;
+    const int64_t pstride = (int64_t)a.kv.n_kv_heads * 2 * P * HD;
+    const bf16_t* kvb = a.kv.kv + a.kv.page_elems(a.layer, 0, kvh, 0);
+
+    // A 32-key block is four regions of 2 HD 16-byte pieces in memory: K and
+    // V^T of its two pages.  Piece q of a region sits at q * 8 elements from
+    // the region's start; in LDS, piece q of K page g is key g*16 + q/(HD/8),
+    // dims (q % (HD/8)) * 8, and piece q of V^T page g is dim q/2, keys
+    // g*16 + (q%2)*8.  Thread t moves pieces t, t + NT, ... of the 8 HD.
+    constexpr int NPC = 8 * HD / NT;  // pieces per thread
+    static_assert(8 * HD % NT == 0 && NT % (2 * HD) == 0 || (2 * HD) % NT == 0, "piece mapping");
+    auto gload = [&](uint4 (&stg)[NPC], int kb) __attribute__((always_inline)) {
+      const int pg0 = trow[kb / P];
+      const int pg1 = (kb + 16 < S) ? trow[kb / P + 1] : pg0;
+#pragma unroll
+      for (int i = 0; i < NPC; ++i) {
+        const int pc = tid + i * NT, reg = pc / (2 * HD), q = pc % (2 * HD);
+        const bf16_t* base = kvb + (int64_t)((reg & 1) ? pg1 : pg0) * pstride + (reg >= 2 ? P * HD : 0);
+        stg[i] = *reinterpret_cast<const uint4*>(base + q * 8);
+      }
+    };
+    // V^T slots past the sequence end are zeroed on the way into LDS
+    auto lstore = [&](int buf, uint4 (&stg)[NPC], int kb) __attribute__((always_inline)) {
+#pragma unroll
+      for (int i = 0; i < NPC; ++i) {
+        const int pc = tid + i * NT, reg = pc / (2 * HD), q = pc % (2 * HD);
+        if (reg < 2) {
+          *reinterpret_cast<uint4*>(&s_k[buf][((reg & 1) * 16 + q / (HD / 8)) * KST + (q % (HD / 8)) * 8]) = stg[i];
+        } else {
+          uint4 v = stg[i];
+          if (kb + 32 > S) v = keep_first(v, min(max(S - (kb + (reg & 1) * 16 + (q & 1) * 8), 0), 8));
+          *reinterpret_cast<uint4*>(&s_v[buf][(q >> 1) * VST + (reg & 1) * 16 + (q & 1) * 8]) = v;
+        }
+      }
+    };
+    // two blocks in flight (register sets A and B) while one is computed
+    uint4 stA[NPC], stB[NPC];
+    if (nb > 0) gload(stA, kbeg);
+    if (nb > 1) gload(stB, kbeg + 32);
+
+    // queries (B operand of S^T) and row positions of this wave's two tiles
+    bf16x8 qf[NRW][KSUB];
+    int rpos[NRW];
+#pragma unroll
+    for (int rt = 0; rt < NRW; ++rt) {
+      const int r = (NRW * w + rt) * 16 + ln;
+      int qrow, h;
+      int64_t prow;
+      rpos[rt] = r < u.nrows ? qpos0 + r / a.G : u.last_pos;
+      if (u.src(a, kvh, r, qrow, h, prow)) {
+        const bf16_t* qp = a.q + (int64_t)qrow * a.q_stride + h * HD + lg * 8;
+#pragma unroll
+        for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + j * 32));
+      } else {
+#pragma unroll
+        for (int j = 0; j < KSUB; ++j) qf[rt][j] = as_bf16x8(make_uint4(0, 0, 0, 0));
+      }
+    }
+    if (nb > 0) lstore(0, stA, kbeg);
+    __syncthreads();
+
+    float m_run[NRW], l_run[NRW];
+    f32x4 o_acc[NDT][NRW];
+#pragma unroll
+    for (int rt = 0; rt < NRW; ++rt) {
+      m_run[rt] = -INFINITY;
+      l_run[rt] = 0.f;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) o_acc[dt][rt] = f32x4{0.f, 0.f, 0.f, 0.f};
+    }
+
+    // masked: the block holds keys above some row's position (wave-uniform)
+    auto compute_block = [&](int buf, int kb, bool masked) __attribute__((always_inline)) {
+      f32x4 sacc[NRW][2];
+#pragma unroll
+      for (int rt = 0; rt < NRW; ++rt) sacc[rt][0] = sacc[rt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < KSUB; ++j) {
+        const bf16x8 k0 = as_bf16x8(*reinterpret_cast<const uint4*>(&s_k[buf][kk0 * KST + j * 32 + lg * 8]));
+        const bf16x8 k1 = as_bf16x8(*reinterpret_cast<const uint4*>(&s_k[buf][(kk0 + 4) * KST + j * 32 + lg * 8]));
+#pragma unroll
+        for (int rt = 0; rt < NRW; ++rt) {
+          sacc[rt][0] = mfma16(k0, qf[rt][j], sacc[rt][0]);
+          sacc[rt][1] = mfma16(k1, qf[rt][j], sacc[rt][1]);
+        }
+      }
+      // keep the V^T fragment reads below the softmax (registers)
+      asm volatile("" ::: "memory");
+      bf16x8 ph[NRW], pl[NRW];
+#pragma unroll
+      for (int rt = 0; rt < NRW; ++rt) {
+        // lane holds S^T[key kb + lg*8 + e][row]
+        float sv[8];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          sv[i] = sacc[rt][0][i];
+          sv[4 + i] = sacc[rt][1][i];
+        }
+        if (masked) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e)
+            if (kb + lg * 8 + e > rpos[rt]) sv[e] = -INFINITY;
+        }
+        float lm = sv[0];
+#pragma unroll
+        for (int e = 1; e < 8; ++e) lm = fmaxf(lm, sv[e]);
+        lm *= a.scale_log2;
+        if (__any(lm > m_run[rt] + 8.f)) {
+          float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
+          mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+          const float m_new = fmaxf(m_run[rt], mx);
+          if (m_new > m_run[rt]) {
+            const float alpha = exp2f(m_run[rt] - m_new);
+            l_run[rt] *= alpha;
+#pragma unroll
+            for (int dt = 0; dt < NDT; ++dt) o_acc[dt][rt] *= alpha;
+            m_run[rt] = m_new;
+          }
+        }
+        const float m_use = m_run[rt] == -INFINITY ? 0.f : m_run[rt];
+        float sum = 0.f;
+        uint32_t hi[4], lo[4];
+#pragma unroll
+        for (int e = 0; e < 8; e += 2) {
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(sv[e], a.scale_log2, -m_use));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(sv[e + 1], a.scale_log2, -m_use));
+          sum += p0 + p1;
+          hi[e / 2] = pack2(p0, p1);
+          lo[e / 2] = pack2(p0 - lo_f(hi[e / 2]), p1 - hi_f(hi[e / 2]));
+        }
+        l_run[rt] += sum;
+        ph[rt] = as_bf16x8(make_uint4(hi[0], hi[1], hi[2], hi[3]));
+        pl[rt] = as_bf16x8(make_uint4(lo[0], lo[1], lo[2], lo[3]));
+      }
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) {
+        const bf16x8 v = as_bf16x8(*reinterpret_cast<const uint4*>(&s_v[buf][(dt * 16 + ln) * VST + lg * 8]));
+#pragma unroll
+        for (int rt = 0; rt < NRW; ++rt) {
+          o_acc[dt][rt] = mfma16(v, ph[rt], o_acc[dt][rt]);
+          o_acc[dt][rt] = mfma16(v, pl[rt], o_acc[dt][rt]);
+        }
+        // at most two V^T fragments in registers at a time
+        if (dt % 2 == 1) asm volatile("" ::: "memory");
+      }
+    };
+    // Block i (keys kbeg + 32 i) is in LDS buffer i % 2 when iteration i
+    // starts; block i + 1 is in flight in one register set, and block i + 2 is
+    // requested into the other, which block i left at the end of iteration i-1.
+    for (int i = 0; i < nb; i += 2) {
+      const int kb = kbeg + 32 * i;
+      if (i + 2 < nb) gload(stA, kb + 64);
+      compute_block(0, kb, i >= nfull);
+      if (i + 1 < nb) lstore(1, stB, kb + 32);
+      __syncthreads();
+      if (i + 1 >= nb) break;
+      if (i + 3 < nb) gload(stB, kb + 96);
+      compute_block(1, kb + 32, i + 1 >= nfull);
+      if (i + 2 < nb) lstore(0, stA, kb + 64);
+      __syncthreads();
+    }
+
+    int next_it = 0;
+    if (tid == 0) next_it = atomicAdd(&a.unit_ctr[cls], 1) * NC + cls;
+    // this wave's rows: partial O, running max and sum
+#pragma unroll
+    for (int rt = 0; rt < NRW; ++rt) {
+      const int r = (NRW * w + rt) * 16 + ln;
+      float l = l_run[rt];
+      l += __shfl_xor(l, 16, 64);
+      l += __shfl_xor(l, 32, 64);
+      int qrow, h;
+      int64_t prow;
+      if (u.src(a, kvh, r, qrow, h, prow)) {
+#pragma unroll
+        for (int dt = 0; dt < NDT; ++dt) {
+          const f32x4 v = o_acc[dt][rt];
+          *reinterpret_cast<float4*>(&a.po[prow * HD + dt * 16 + lg * 4]) = make_float4(v[0], v[1], v[2], v[3]);
+        }
+        if (lg == 0) {
+          a.pm[prow] = m_run[rt];
+          a.pl[prow] = l;
+        }
+      }
+    }
+    if (tid == 0) s_it = next_it;
+    __syncthreads();
+  }
+}
+
 // Merge a (request, row block)'s chunk partials in item order; o = sum / l -> bf16.
 // Workgroup = (segment, kv-head, slice of 1024/HD rows: 8 at head_dim 128), so
 // a step's merge spreads over hundreds of workgroups.  One wave per row puts
@@ -538,6 +802,11 @@ int attn_rows_per_block(int G, int k_rows) {
 }
 
 void launch_attn(const AttnArgs& a, int RB, int head_dim, int grid, hipStream_t st) {
+  if (RB == 128) {  // prefill row blocks
+    if (head_dim == 128) k_attn_rows<4, 128><<<grid, 256, 0, st>>>(a);
+    else k_attn_rows<4, 64><<<grid, 256, 0, st>>>(a);
+    return;
+  }
   if (RB == 16)
     launch_attn_nr<1>(a, head_dim, grid, st);
   else if (RB == 32)
@@ -547,7 +816,9 @@ void launch_attn(const AttnArgs& a, int RB, int head_dim, int grid, hipStream_t 
 }
 
 void launch_attn_combine(const AttnArgs& a, int RB, int head_dim, int n_segs, hipStream_t st) {
-  if (RB == 16)
+  if (RB == 128)
+    launch_comb<128>(a, head_dim, n_segs, st);
+  else if (RB == 16)
     launch_comb<16>(a, head_dim, n_segs, st);
   else if (RB == 32)
     launch_comb<32>(a, head_dim, n_segs, st);

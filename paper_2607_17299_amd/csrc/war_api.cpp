@@ -86,7 +86,8 @@ struct Profiler {
     return pool[used++];
   }
 };
-constexpr int kPrefillChunk = 2048;  // keys per attention item when prefilling (chunk-major: L2 serves the row blocks)
+constexpr int kPrefillChunk = 4096;  // keys per attention item when prefilling (chunk-major: L2 serves the row blocks)
+constexpr int kPrefillRows = 128;    // attention rows per prefill row block (k_attn_rows)
 constexpr int kMaxItemsPerSeq = 512;  // attention chunks one combine merges
 constexpr int kAttnGrid = 512;        // persistent attention grid: 2 workgroups per CU
 constexpr int64_t kPartialCap = int64_t(64) << 20;  // fp32 split-K partial elements
@@ -1171,8 +1172,10 @@ war_status war_prefill_append(war_model* m, war_kv_pool* p, int32_t n, const int
   HIPCHK(hipGetLastError());
   set_exact_free(p, fc - need);
 
-  // forward over chunks of at most max_rows packed rows
-  const int RB = 48;
+  // forward over chunks of at most max_rows packed rows; attention in row
+  // blocks of kPrefillRows rows (k_attn_rows)
+  const int RB = kPrefillRows;
+  CHECK(RB % G == 0, "internal: query heads per kv head must divide the prefill row block");
   const int TB = RB / G;
   int chunk = kPrefillChunk;
   while (cdiv_i(p->dev.max_pages * P, chunk) > kMaxItemsPerSeq) chunk *= 2;
