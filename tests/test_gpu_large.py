@@ -377,17 +377,19 @@ def _full_size_check(st, kv_seed, sample, tag, setup=None, chunk=None):
 @ORACLE_SLOW
 def test_full_size_low_load_sampled():
     """The benchmark's workload at full size (36 layers, 8 x 32768, k = 8);
-    request 0 is recomputed by the oracle.  The batch has enough keys for
-    2048-key attention chunks (8 x 17 items), so those are what it checks."""
-    _full_size_check(harness.low_load_step(), 5, [0], "low_load", chunk=2048)
+    requests 0 and 7 are recomputed by the oracle.  The batch has enough keys
+    for 2048-key attention chunks (8 x 17 items), so those are what it checks."""
+    _full_size_check(harness.low_load_step(), 5, [0, 7], "low_load", chunk=2048)
 
 
 @ORACLE_SLOW
 def test_full_size_high_load_sampled():
     """64 requests with lognormal contexts and k = 0 (plain batched decode);
-    the shortest and the longest request are recomputed by the oracle."""
+    the shortest, the median and the longest request are recomputed by the
+    oracle."""
     st = harness.high_load_step(k=0)
-    sample = [int(np.argmin(st.ctx_lens)), int(np.argmax(st.ctx_lens))]
+    order = np.argsort(st.ctx_lens, kind="stable")
+    sample = [int(order[0]), int(order[len(order) // 2]), int(order[-1])]
     _full_size_check(st, 5, sample, "high_load")
 
 
@@ -450,6 +452,75 @@ def test_full_size_high_load_k2_sampled():
         drafts[b] = d
     st = harness.Step(st.seq_ids, st.ctx_lens, st.last_tokens, drafts, 2)
     _full_size_check(st, 5, sample, "high_load_k2")
+
+
+@ORACLE_SLOW
+def test_full_size_tree_sampled():
+    """Tree drafts at full depth (36 layers, full widths): 4 requests over
+    seeded contexts with 4-node trees.  Request 0's root has the oracle's own
+    greedy token as its second child (with a grandchild), so the GPU must
+    accept that branch; request 2 carries a random tree.  Both are recomputed
+    by the oracle node by node (every node's root path decoded as a chain),
+    with the bound from the fp32 drift of the deepest path; request 0's
+    committed cache (last layer) must be the accepted path's K/V."""
+    war = _war()
+    cfg = synth.LARGE
+    w = harness.large_weights(cfg)
+    model = war.Model(cfg, w, max_rows=64)
+    W = Weights(cfg, w, cache=True)
+    kv_seed = 5
+    ctxs = np.array([3000, 4500, 1200, 6000], np.int32)
+    B = len(ctxs)
+    last = synth.uniform_tokens(70, B, cfg.vocab)
+    rng = np.random.default_rng(70)
+
+    def kv_of(b):
+        layers = []
+        for l in range(cfg.n_layers):
+            a = synth.kv_context(cfg, kv_seed, b, l, 0, int(ctxs[b]), "cuda").cpu().double().numpy()
+            layers.append((a[0], a[1]))
+        return RequestKV(cfg, layers)
+    kv0 = kv_of(0)
+    z, _ = forward_block(cfg, W, [int(last[0])], int(ctxs[0]), kv0.get)
+    from oracle.accept import argmax_lowest
+    g0 = int(argmax_lowest(z)[0])
+    rnd = [[int(v) for v in rng.integers(0, cfg.vocab, 4)] for _ in range(B)]
+    drafts = [[rnd[0][0], g0, rnd[0][1], rnd[0][2]], rnd[1], rnd[2], rnd[3]]
+    parents = [[0, 0, 2, 1], [0, 1, 1, 0], [0, 1, 1, 0], [0, 0, 0, 0]]
+    st = harness.Step(np.arange(B, dtype=np.int32), ctxs, last, drafts, 4, parents)
+    pool = harness.make_pool(cfg, st.ctx_lens, 6)
+    harness.load_contexts(pool, cfg, st.ctx_lens, st.seq_ids, kv_seed)
+    ds = harness.DeviceStep(st, with_logits=True, vocab=cfg.vocab)
+    ds.verify_tree(model, pool, logits=True)
+    ds.commit(pool, discard=False)
+    torch.cuda.synchronize()
+    glog = ds.logits.cpu().numpy().reshape(B, 5, cfg.vocab)
+    acc, nxt, path = ds.accept.cpu().numpy(), ds.next.cpu().numpy(), ds.path.cpu().numpy()
+    np.testing.assert_array_equal(ds.ctx.cpu().numpy(), st.ctx_lens + acc + 1)
+    report, out = [], []
+    for b, kv in ((0, kv0), (2, kv_of(2))):
+        tag = f"full-size tree req {b}"
+        r = verify_tree_request(cfg, W, kv, int(last[b]), drafts[b], parents[b])
+        # the deepest root path: nodes 2, 3 (request 0) or 1, 2 (request 2)
+        deep = [int(last[b])] + ([drafts[b][1], drafts[b][2]] if b == 0 else [drafts[b][0], drafts[b][1]])
+        o64, kv64 = forward_block(cfg, W, deep, int(ctxs[b]), kv.get)
+        o32, kv32 = forward_block(cfg, W, deep, int(ctxs[b]), kv.get, precision="fp32")
+        tol = fp32_drift_tol(o64, o32)
+        L = cfg.n_layers - 1
+        kv_tol = max(3e-2, 1.5 * max(float(np.abs(kv64[L][i] - kv32[L][i]).max()) for i in (0, 1)))
+        a = int(acc[b])
+        same = compare_tree_request(r, glog[b], [int(last[b])] + drafts[b], parents[b], a, int(nxt[b]),
+                                    path[b, :a], report, tag, tol=tol)
+        out.append((b, a, [int(x) for x in path[b, :a]], round(tol, 4), round(kv_tol, 4)))
+        if b == 0:
+            # the planted greedy child is accepted unless the root is a near-tie
+            assert a >= 1 or report, (tag, a)
+        if same:
+            g = pool.gather_kv(b, int(ctxs[b]) + a + 1, L).double().cpu().numpy()
+            nk, nv = r["new_kv"][L]
+            np.testing.assert_allclose(g[0][:, ctxs[b]:], nk, atol=kv_tol, err_msg=tag)
+            np.testing.assert_allclose(g[1][:, ctxs[b]:], nv, atol=kv_tol, err_msg=tag)
+    print(f"\nfull-size tree: (request, GPU accept, path, logit bound, kv bound) {out}; {report}")
 
 
 @ORACLE_SLOW
