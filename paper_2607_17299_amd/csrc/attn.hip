@@ -292,19 +292,20 @@ k_attn(AttnArgs a) {
 #pragma unroll
         for (int e = 1; e < 8; ++e) lm = fmaxf(lm, sv[e]);
         lm *= a.scale_log2;
-        // Lazy rescaling: the running max only moves when a score exceeds it by
-        // more than 2^8 (weights stay below 256, exact in fp32); the decision is
-        // taken for the whole wave so the 4 lanes of a row always agree.
+        // Lazy rescaling: a row's running max only moves when one of its scores
+        // exceeds it by more than 2^8 (weights stay below 256, exact in fp32).
+        // Each row decides from its own maximum (the 4 lanes of a row agree), so
+        // a row's result never depends on the other rows of its tile; the wave
+        // skips the row maxima when no lane needs them.
         if (__any(lm > m_run[rt] + 8.f)) {
           float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
           mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-          const float m_new = fmaxf(m_run[rt], mx);
-          if (m_new > m_run[rt]) {
-            const float alpha = exp2f(m_run[rt] - m_new);
+          if (mx > m_run[rt] + 8.f) {
+            const float alpha = exp2f(m_run[rt] - mx);
             l_run[rt] *= alpha;
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) o_acc[dt][rt] *= alpha;
-            m_run[rt] = m_new;
+            m_run[rt] = mx;
           }
         }
         const float m_use = m_run[rt] == -INFINITY ? 0.f : m_run[rt];
@@ -618,16 +619,16 @@ k_attn_rows(AttnArgs a) {
 #pragma unroll
         for (int e = 1; e < 8; ++e) lm = fmaxf(lm, sv[e]);
         lm *= a.scale_log2;
+        // lazy rescaling, decided per row as in k_attn
         if (__any(lm > m_run[rt] + 8.f)) {
           float mx = fmaxf(lm, __shfl_xor(lm, 16, 64));
           mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-          const float m_new = fmaxf(m_run[rt], mx);
-          if (m_new > m_run[rt]) {
-            const float alpha = exp2f(m_run[rt] - m_new);
+          if (mx > m_run[rt] + 8.f) {
+            const float alpha = exp2f(m_run[rt] - mx);
             l_run[rt] *= alpha;
 #pragma unroll
             for (int dt = 0; dt < NDT; ++dt) o_acc[dt][rt] *= alpha;
-            m_run[rt] = m_new;
+            m_run[rt] = mx;
           }
         }
         const float m_use = m_run[rt] == -INFINITY ? 0.f : m_run[rt];

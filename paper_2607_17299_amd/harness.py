@@ -222,20 +222,34 @@ def high_load_step(seed: int = 0, B: int = 64, k: int = 0, vocab: int = 151936,
 
 def teacher_continuation(model: war.Model, pool: war.Pool, st: Step, n: int) -> List[List[int]]:
     """The target's own greedy continuation of each request (n tokens after the
-    pending token), by n verify steps that feed back the known prefix and
-    discard: the state of the pool is unchanged afterwards."""
+    pending token), by verify steps that feed back the known prefix and
+    discard: the state of the pool is unchanged afterwards.  Every step has
+    the same shape (n drafts per request, the unknown tail padded), so a row's
+    logits do not depend on the step (steps of different shapes sum in other
+    orders and may disagree on an argmax at a near-tie).  Should a fed-back
+    prefix still not be accepted in full, the request continues from that
+    step's own decision."""
+    vocab = model.cfg.vocab
     cont: List[List[int]] = [[] for _ in range(st.B)]
-    for j in range(n):
-        s = Step(st.seq_ids, st.ctx_lens, st.last_tokens, [c[:j] for c in cont], max(j, 1))
-        ds = DeviceStep(s)
+    for _ in range(2 * n + 2):
+        if all(len(c) >= n for c in cont):
+            break
+        drafts = [c[:n] + [(int(st.last_tokens[b]) + 1 + i) % vocab for i in range(n - min(len(c), n))]
+                  for b, c in enumerate(cont)]
+        ds = DeviceStep(Step(st.seq_ids, st.ctx_lens, st.last_tokens, drafts, n))
         ds.verify(model, pool)
         ds.commit(pool, discard=True)
         nxt = ds.next.cpu().numpy()
         acc = ds.accept.cpu().numpy()
         for b in range(st.B):
-            assert acc[b] == j
-            cont[b].append(int(nxt[b]))
-    return cont
+            j, a = len(cont[b]), int(acc[b])
+            if j >= n:
+                continue
+            # accepted drafts beyond the known prefix (pads that happen to be
+            # greedy) are part of the greedy stream too
+            cont[b] = drafts[b][:a] + [int(nxt[b])] if a >= j else cont[b][:a] + [int(nxt[b])]
+    assert all(len(c) >= n for c in cont), "the greedy continuation did not settle"
+    return [c[:n] for c in cont]
 
 
 def corrupt(drafts: List[List[int]], p: float, seed: int, vocab: int) -> List[List[int]]:

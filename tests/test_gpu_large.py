@@ -100,6 +100,38 @@ def test_reduced_depth_verify_matches_oracle(large2, k, lens, ctxs):
     print(f"\nk={k}: max logit err {err:.3e}; reported {report}")
 
 
+@pytest.mark.parametrize("k", [2, 4, 8])
+def test_rows_do_not_depend_on_later_drafts(large2, k):
+    """A row's result depends only on the tokens up to it: changing only the
+    last draft token (the input of the last row) of one request leaves every
+    earlier row's logits bitwise unchanged, for one, two and three row tiles
+    and across key chunks.  (The attention's lazy rescaling is decided per row,
+    so no row's rounding follows another row's rescale events.)"""
+    cfg, model = large2["cfg"], large2["model"]
+    ctxs = np.array([2100, 900, 4500, 3333], np.int32)
+    B = len(ctxs)
+    rng = np.random.default_rng(300 + k)
+    last = synth.uniform_tokens(300 + k, B, cfg.vocab)
+    drafts = [[int(v) for v in rng.integers(0, cfg.vocab, k)] for _ in range(B)]
+    pool = harness.make_pool(cfg, ctxs, k + 2)
+    harness.load_contexts(pool, cfg, ctxs, np.arange(B), KV_SEED)
+    out = []
+    for variant in range(2):
+        d = [list(x) for x in drafts]
+        if variant:
+            d[1][-1] = (d[1][-1] + 12345) % cfg.vocab
+        ds = harness.DeviceStep(harness.Step(np.arange(B, dtype=np.int32), ctxs, last, d, k),
+                                with_logits=True, vocab=cfg.vocab)
+        ds.verify(model, pool, logits=True)
+        ds.commit(pool, discard=True)
+        torch.cuda.synchronize()
+        out.append(ds.logits.cpu().numpy().reshape(B, k + 1, cfg.vocab))
+    for b in range(B):
+        rows = k if b == 1 else k + 1   # request 1's last row saw the changed token
+        np.testing.assert_array_equal(out[0][b, :rows], out[1][b, :rows], err_msg=f"k={k} req {b}")
+    assert not np.array_equal(out[0][1, k], out[1][1, k])
+
+
 @pytest.mark.parametrize("k", [3, 11])
 def test_reduced_depth_tree_matches_oracle(large2, k):
     """Tree drafts on the 36-layer shapes (2 layers): random trees of ragged
