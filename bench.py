@@ -52,6 +52,9 @@ def parse():
     ap.add_argument("--no-variants", action="store_true")
     ap.add_argument("--sweep", action="store_true",
                     help="only the speculation on/off sweep: step time over batch size x draft length")
+    ap.add_argument("--library-gemm", action="store_true",
+                    help="time the vendor GEMM (torch.matmul, hipBLASLt) on the step's projection shapes "
+                         "at 72 and 192 rows, weights rotated past the memory-side cache, and exit")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only time a plain 2 GiB device copy (counter calibration)")
     return ap.parse_args()
@@ -378,6 +381,43 @@ def time_variant(ds, model, pool, steps, uniforms=None):
             "accept_lens": acc.tolist()}
 
 
+def library_gemm():
+    """The vendor GEMM on the decoder's projection shapes (plain bf16 matmul,
+    no epilogue), each weight matrix rotated over enough copies (up to 2.2 GB)
+    that no launch finds it in the memory-side cache, as in a decode step."""
+    import torch
+    from paper_2607_17299_amd import synth
+    cfg = synth.LARGE
+    d, f, v = cfg.d_model, cfg.ffn_dim, cfg.vocab
+    qkv = (cfg.n_q_heads + 2 * cfg.n_kv_heads) * cfg.head_dim
+    shapes = {"qkv": (qkv, d), "o": (d, cfg.n_q_heads * cfg.head_dim), "gate_up": (2 * f, d),
+              "down": (d, f), "lm_head": (v, d)}
+    out = {"what": "torch.matmul (hipBLASLt) bf16, A [M][K] x W[N][K]^T, weights rotated", "us_per_launch": {}}
+    g = torch.Generator(device="cuda")
+    g.manual_seed(0)
+    for M in (72, 192):
+        for name, (N, K) in shapes.items():
+            ncopy = max(1, min(24, int(2.2e9 // (N * K * 2))))
+            Ws = [torch.randn(N, K, device="cuda", dtype=torch.bfloat16, generator=g) for _ in range(ncopy)]
+            A = torch.randn(M, K, device="cuda", dtype=torch.bfloat16, generator=g)
+            for i in range(ncopy):
+                torch.matmul(A, Ws[i].t())
+            torch.cuda.synchronize()
+            reps = max(ncopy, 24)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for i in range(reps):
+                torch.matmul(A, Ws[i % ncopy].t())
+            e1.record()
+            torch.cuda.synchronize()
+            us = e0.elapsed_time(e1) * 1e3 / reps
+            out["us_per_launch"][f"M{M}_{name}"] = {"us": round(us, 2), "copies": ncopy,
+                                                    "frac_of_8TBps": round(N * K * 2 / us / 1e3 / HBM_PEAK_GBPS, 4)}
+            del Ws
+            torch.cuda.empty_cache()
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -385,6 +425,10 @@ def main():
                           "n_gpus": args.gpus}))
         sys.exit(2)
     import torch
+
+    if args.library_gemm:
+        print(json.dumps(library_gemm()), flush=True)
+        return
 
     if args.copy_probe:
         n = 1 << 30                                   # 2 GiB of bf16 each way
