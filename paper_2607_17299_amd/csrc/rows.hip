@@ -79,7 +79,11 @@ __device__ __forceinline__ float4 sum_splits(const float* P, int64_t sstride, in
   return x;
 }
 
-// h += sum_s P[s]; u = norm(h) * g   (one 1024-thread workgroup per row)
+// h += sum_s P[s]; u = norm(h) * g   (one 1024-thread workgroup per row).
+// NV > 0: each thread keeps its NV float4 of the row in registers (d <= 4096 NV)
+// and has its gains loaded before the reduction, so the normalisation needs no
+// second pass over memory; NV = 0: any width, h re-read after the reduction.
+template <int NV>
 __global__ void __launch_bounds__(1024) k_residual_norm(int rows, int splits, const float* P, int d,
                                                         const bf16_t* g, float eps, float* h,
                                                         bf16_t* u) {
@@ -88,19 +92,47 @@ __global__ void __launch_bounds__(1024) k_residual_norm(int rows, int splits, co
   float* hr = h + (int64_t)r * d;
   const int64_t sstride = (int64_t)rows * d;
   float ss = 0.f;
-  for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
-    float4 x = *reinterpret_cast<const float4*>(hr + c);
-    x = sum_splits(P + (int64_t)r * d + c, sstride, splits, x);
-    ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
-    *reinterpret_cast<float4*>(hr + c) = x;
+  if constexpr (NV == 0) {
+    for (int c = threadIdx.x * 4; c < d; c += blockDim.x * 4) {
+      float4 x = *reinterpret_cast<const float4*>(hr + c);
+      x = sum_splits(P + (int64_t)r * d + c, sstride, splits, x);
+      ss += x.x * x.x + x.y * x.y + x.z * x.z + x.w * x.w;
+      *reinterpret_cast<float4*>(hr + c) = x;
+    }
+    norm_row(hr, d, g, eps, u + (int64_t)r * d, ss, red);
+  } else {
+    float4 x[NV];
+    uint2 gg[NV];
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = (threadIdx.x + i * 1024) * 4;
+      if (c < d) {
+        gg[i] = *reinterpret_cast<const uint2*>(g + c);
+        x[i] = sum_splits(P + (int64_t)r * d + c, sstride, splits, *reinterpret_cast<const float4*>(hr + c));
+        ss += x[i].x * x[i].x + x[i].y * x[i].y + x[i].z * x[i].z + x[i].w * x[i].w;
+        *reinterpret_cast<float4*>(hr + c) = x[i];
+      }
+    }
+    const float rs = rsqrtf(block_sum(ss, red) / (float)d + eps);
+    bf16_t* ur = u + (int64_t)r * d;
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int c = (threadIdx.x + i * 1024) * 4;
+      if (c < d) {
+        uint2 o;
+        o.x = pack2(x[i].x * rs * bf2f(gg[i].x & 0xffff), x[i].y * rs * bf2f(gg[i].x >> 16));
+        o.y = pack2(x[i].z * rs * bf2f(gg[i].y & 0xffff), x[i].w * rs * bf2f(gg[i].y >> 16));
+        *reinterpret_cast<uint2*>(ur + c) = o;
+      }
+    }
   }
-  norm_row(hr, d, g, eps, u + (int64_t)r * d, ss, red);
 }
 
 // Sum the QKV partials of one row, rotate q and k (rotate-half pairs (j, j+D/2)),
 // round to bf16; q goes to its buffer, k and v of active rows into the KV page slot
 // of the row's position (a tree node's own slot, when the step has tree drafts).
-__global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const float* P, ModelDims md,
+// Each thread takes four consecutive pairs (16-byte loads of the partials).
+__global__ void __launch_bounds__(64) k_qkv_rope(int rows, int splits, const float* P, ModelDims md,
                                                   const float* cos_t, const float* sin_t,
                                                   StepMeta meta, const int32_t* row_req,
                                                   const int32_t* table, int max_pages, KvGeom kv,
@@ -110,7 +142,7 @@ __global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const fl
   const int nq_pairs = md.nq * half, nk_pairs = md.nkv * half;
   const int n_pairs = md.qkv / 2;
   const bool act = meta.active[r] != 0;
-  const int p = blockIdx.y * blockDim.x + threadIdx.x;
+  const int p = (blockIdx.y * blockDim.x + threadIdx.x) * 4;  // first of four pairs
   if (p >= n_pairs) return;
   int page = 0, slot = 0;
   if (act) {
@@ -121,48 +153,64 @@ __global__ void __launch_bounds__(256) k_qkv_rope(int rows, int splits, const fl
   }
   const float* pr = P + (int64_t)r * md.qkv;
   const int64_t pstride = (int64_t)rows * md.qkv;
-  {
-    int region, head, j;
-    if (p < nq_pairs) {
-      region = 0;
-      head = p / half;
-      j = p % half;
-    } else if (p < nq_pairs + nk_pairs) {
-      region = 1;
-      head = (p - nq_pairs) / half;
-      j = (p - nq_pairs) % half;
+  int region, head, j;
+  if (p < nq_pairs) {
+    region = 0;
+    head = p / half;
+    j = p % half;
+  } else if (p < nq_pairs + nk_pairs) {
+    region = 1;
+    head = (p - nq_pairs) / half;
+    j = (p - nq_pairs) % half;
+  } else {
+    region = 2;
+    head = (p - nq_pairs - nk_pairs) / half;
+    j = (p - nq_pairs - nk_pairs) % half;
+  }
+  const int col = (region == 0 ? 0 : region == 1 ? md.nq * md.hd : (md.nq + md.nkv) * md.hd) +
+                  head * md.hd + j;
+  float x1[4] = {0.f, 0.f, 0.f, 0.f}, x2[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int s = 0; s < splits; ++s) {
+    const float4 a1 = *reinterpret_cast<const float4*>(pr + s * pstride + col);
+    const float4 a2 = *reinterpret_cast<const float4*>(pr + s * pstride + col + half);
+    x1[0] += a1.x; x1[1] += a1.y; x1[2] += a1.z; x1[3] += a1.w;
+    x2[0] += a2.x; x2[1] += a2.y; x2[2] += a2.z; x2[3] += a2.w;
+  }
+  bf16_t b1[4], b2[4];
+  if (region < 2) {
+    const float4 c = *reinterpret_cast<const float4*>(cos_t + r * half + j);
+    const float4 sn = *reinterpret_cast<const float4*>(sin_t + r * half + j);
+    const float cc[4] = {c.x, c.y, c.z, c.w}, ss[4] = {sn.x, sn.y, sn.z, sn.w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      b1[e] = f2bf(x1[e] * cc[e] - x2[e] * ss[e]);
+      b2[e] = f2bf(x2[e] * cc[e] + x1[e] * ss[e]);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      b1[e] = f2bf(x1[e]);
+      b2[e] = f2bf(x2[e]);
+    }
+  }
+  auto pack4 = [](const bf16_t* v) {
+    return make_uint2((uint32_t)v[0] | ((uint32_t)v[1] << 16), (uint32_t)v[2] | ((uint32_t)v[3] << 16));
+  };
+  if (region == 0) {
+    bf16_t* qr = q + (int64_t)r * md.nq * md.hd + head * md.hd;
+    *reinterpret_cast<uint2*>(qr + j) = pack4(b1);
+    *reinterpret_cast<uint2*>(qr + j + half) = pack4(b2);
+  } else if (act) {
+    bf16_t* base = kv.kv + kv.page_elems(layer, page, head, region - 1);
+    if (region == 1) {
+      *reinterpret_cast<uint2*>(base + slot * md.hd + j) = pack4(b1);
+      *reinterpret_cast<uint2*>(base + slot * md.hd + j + half) = pack4(b2);
     } else {
-      region = 2;
-      head = (p - nq_pairs - nk_pairs) / half;
-      j = (p - nq_pairs - nk_pairs) % half;
-    }
-    const int col = (region == 0 ? 0 : region == 1 ? md.nq * md.hd : (md.nq + md.nkv) * md.hd) +
-                    head * md.hd + j;
-    float x1 = 0.f, x2 = 0.f;
-#pragma unroll 8
-    for (int s = 0; s < splits; ++s) {
-      x1 += pr[s * pstride + col];
-      x2 += pr[s * pstride + col + half];
-    }
-    float y1 = x1, y2 = x2;
-    if (region < 2) {
-      const float c = cos_t[r * half + j], sn = sin_t[r * half + j];
-      y1 = x1 * c - x2 * sn;
-      y2 = x2 * c + x1 * sn;
-    }
-    const bf16_t b1 = f2bf(y1), b2 = f2bf(y2);
-    if (region == 0) {
-      bf16_t* qr = q + (int64_t)r * md.nq * md.hd + head * md.hd;
-      qr[j] = b1;
-      qr[j + half] = b2;
-    } else if (act) {
-      bf16_t* base = kv.kv + kv.page_elems(layer, page, head, region - 1);
-      if (region == 1) {
-        base[slot * md.hd + j] = b1;
-        base[slot * md.hd + j + half] = b2;
-      } else {
-        base[j * kv.page_size + slot] = b1;
-        base[(j + half) * kv.page_size + slot] = b2;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        base[(j + e) * kv.page_size + slot] = b1[e];
+        base[(j + e + half) * kv.page_size + slot] = b2[e];
       }
     }
   }
@@ -301,14 +349,19 @@ void launch_embed_norm(int rows, const int32_t* tok, const bf16_t* E, const bf16
 }
 void launch_residual_norm(int rows, int splits, const float* P, int d, const bf16_t* g, float eps,
                           float* h, bf16_t* u, hipStream_t st) {
-  k_residual_norm<<<rows, 1024, 0, st>>>(rows, splits, P, d, g, eps, h, u);
+  if (d <= 4096)
+    k_residual_norm<1><<<rows, 1024, 0, st>>>(rows, splits, P, d, g, eps, h, u);
+  else if (d <= 8192)
+    k_residual_norm<2><<<rows, 1024, 0, st>>>(rows, splits, P, d, g, eps, h, u);
+  else
+    k_residual_norm<0><<<rows, 1024, 0, st>>>(rows, splits, P, d, g, eps, h, u);
 }
 void launch_qkv_rope(int rows, int splits, const float* P, const ModelDims& md,
                      const float* cos_t, const float* sin_t, const StepMeta& meta,
                      const int32_t* row_req, const int32_t* table, int max_pages, const KvGeom& kv,
                      int layer, bf16_t* q, hipStream_t st) {
-  dim3 grid(rows, cdiv_i(md.qkv / 2, 256));
-  k_qkv_rope<<<grid, 256, 0, st>>>(rows, splits, P, md, cos_t, sin_t, meta, row_req, table,
+  dim3 grid(rows, cdiv_i(md.qkv / 8, 64));  // four pairs per thread, one wave per workgroup
+  k_qkv_rope<<<grid, 64, 0, st>>>(rows, splits, P, md, cos_t, sin_t, meta, row_req, table,
                                    max_pages, kv, layer, q);
 }
 void launch_argmax_accept(int n_req, const int32_t* ntok, int row_stride, int n_blocks,
