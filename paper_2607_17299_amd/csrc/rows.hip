@@ -221,24 +221,23 @@ __global__ void __launch_bounds__(64) k_qkv_rope(int rows, int splits, const flo
 // draft prefix that matches.  Tree drafts: a node is accepted when its parent
 // is and its token is the parent's greedy token; the deepest accepted node
 // (lowest index among equals) ends the accepted path.
-__global__ void __launch_bounds__(256) k_argmax_accept(const int32_t* ntok, int row_stride,
+__global__ void __launch_bounds__(1024) k_argmax_accept(const int32_t* ntok, int row_stride,
                                                        int n_blocks, const float* amax_v,
                                                        const int32_t* amax_i,
                                                        const int32_t* drafts, const int32_t* parents,
                                                        int k_max, int32_t* accept_lens, int32_t* next_tokens,
                                                        int32_t* accept_path) {
-  __shared__ float sv[4];
-  __shared__ int si[4];
   __shared__ int greedy[64];
   __shared__ int s_par[64], s_dep[64], s_ok[64];
   const int b = blockIdx.x;
   const int n = ntok ? min(ntok[b], 64) : 1;
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  for (int i = 0; i < n; ++i) {
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  // one wave per row (rows w, w + nw, ...): the rows' reductions run side by side
+  for (int i = w; i < n; i += nw) {
     const int64_t row = (int64_t)b * row_stride + i;
     float v = -INFINITY;
     int idx = 0x7fffffff;
-    for (int c = threadIdx.x; c < n_blocks; c += blockDim.x) {
+    for (int c = lane; c < n_blocks; c += 64) {
       const float ov = amax_v[row * n_blocks + c];
       const int oi = amax_i[row * n_blocks + c];
       if (ov > v || (ov == v && oi < idx)) {
@@ -255,21 +254,9 @@ __global__ void __launch_bounds__(256) k_argmax_accept(const int32_t* ntok, int 
         idx = oi;
       }
     }
-    if (lane == 0) {
-      sv[w] = v;
-      si[w] = idx;
-    }
-    __syncthreads();
-    if (threadIdx.x == 0) {
-      for (int ww = 1; ww < 4; ++ww)
-        if (sv[ww] > v || (sv[ww] == v && si[ww] < idx)) {
-          v = sv[ww];
-          idx = si[ww];
-        }
-      greedy[i] = idx;
-    }
-    __syncthreads();
+    if (lane == 0) greedy[i] = idx;
   }
+  __syncthreads();
   if (threadIdx.x != 0) return;
   int a = 0, last = 0;
   if (parents && n > 0) {
@@ -368,7 +355,7 @@ void launch_argmax_accept(int n_req, const int32_t* ntok, int row_stride, int n_
                           const float* amax_v, const int32_t* amax_i, const int32_t* draft_tokens,
                           const int32_t* parents, int k_max, int32_t* accept_lens, int32_t* next_tokens,
                           int32_t* accept_path, hipStream_t st) {
-  k_argmax_accept<<<n_req, 256, 0, st>>>(ntok, row_stride, n_blocks, amax_v, amax_i, draft_tokens,
+  k_argmax_accept<<<n_req, 1024, 0, st>>>(ntok, row_stride, n_blocks, amax_v, amax_i, draft_tokens,
                                          parents, k_max, accept_lens, next_tokens, accept_path);
 }
 void launch_kv_compact(const KvGeom& kv, int n_layers, int B, const StepMeta& meta, const int32_t* table,
