@@ -353,16 +353,17 @@ struct Timed {
   }
 };
 
-// Split-K: the largest step count per split (16, 12, 8 or 4 steps of 64) that
-// divides K exactly and still gives >= 192 workgroups; the fully unrolled
-// kernels need exact splits.  Fewer splits mean fewer fp32 partial sums to
-// write and to add up afterwards; below ~192 workgroups too few CUs stream W
-// (measured on the 4096- and 6144-wide projections: 192-256 is the optimum).
+// Split-K: the fewest splits that divide K exactly, give >= 192 workgroups and
+// leave at most 48 steps of 64 per split; the fully unrolled kernels need exact
+// splits.  Fewer splits mean fewer fp32 partial sums to write and to add up
+// afterwards; below ~192 workgroups too few CUs stream W (measured on the
+// 4096- and 6144-wide projections: 192-256 is the optimum); at 512-1024 rows
+// (prefill chunks) splits of 64-192 steps ran 6-25% slower than 32-48.
 Split pick_split(int M, int N, int K, int64_t cap_elems) {
   const int base = (N / 128) * gemm_mblock_groups(M);  // workgroups per split
   for (int s = 1; s <= 64; ++s) {
     if (K % (s * 64)) continue;
-    if ((int64_t)base * s >= 192 && (int64_t)s * M * N <= cap_elems) return {s, K / s};
+    if ((int64_t)base * s >= 192 && K / (s * 64) <= 48 && (int64_t)s * M * N <= cap_elems) return {s, K / s};
   }
   // fall back: one split per 1024 of K (runtime-loop kernel)
   int s = std::max(1, K / 1024);
