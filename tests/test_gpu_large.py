@@ -24,7 +24,7 @@ import torch
 from oracle.decoder import RequestKV, Weights, forward_block
 from oracle.verify import greedy_decode, prefill_request, verify_request, verify_tree_request
 from paper_2607_17299_amd import harness, synth
-from parity import compare_request, compare_tree_request, fp32_drift_tol, shared_units
+from parity import NEAR_TIE, compare_request, compare_tree_request, fp32_drift_tol, shared_units
 
 pytestmark = pytest.mark.gpu
 KV_SEED = 9
@@ -235,10 +235,15 @@ def test_reduced_depth_sibling_drafts_accepted(large2):
     assert ds.next.cpu().tolist() == [d[k] for d in drafts]
 
 
-def test_reduced_depth_prefill_append(large2):
+@pytest.mark.parametrize("ctxs,n_new", [([512, 96], [300, 45]), ([77, 4000], [1, 33]), ([1024, 333], [64, 129])])
+def test_reduced_depth_prefill_append(large2, ctxs, n_new):
+    """war_prefill_append at full widths (2 layers): the last row's logits and
+    next token, and the appended K/V, against the oracle.  Lengths cover one
+    token, a 32-token row block plus one (the prefill attention's row blocks
+    hold 32 tokens x 4 query heads), exact multiples, several row blocks, and
+    contexts that end inside a page."""
     war, cfg, model, W = large2["war"], large2["cfg"], large2["model"], large2["W"]
-    ctxs = np.array([512, 96], np.int32)
-    n_new = [300, 45]
+    ctxs = np.array(ctxs, np.int32)
     pool = harness.make_pool(cfg, ctxs + np.array(n_new), 8)
     harness.load_contexts(pool, cfg, ctxs, [0, 1], KV_SEED)
     toks = [synth.uniform_tokens(70 + b, n, cfg.vocab) for b, n in enumerate(n_new)]
@@ -256,7 +261,7 @@ def test_reduced_depth_prefill_append(large2):
         assert err < 5e-2, err
         if int(nxt[b]) != r["next"]:
             s = np.sort(r["logits"][-1])
-            assert s[-1] - s[-2] <= 2 * err
+            assert s[-1] - s[-2] < NEAR_TIE and s[-1] - s[-2] <= 2 * err, (b, s[-1] - s[-2], err)
         g = pool.gather_kv(b, int(ctxs[b]) + n_new[b], 1).double().cpu().numpy()
         K, V = kv.get(1)
         np.testing.assert_allclose(g[0][:, ctxs[b]:], K[:, ctxs[b]:], atol=3e-2, rtol=2e-2)

@@ -15,7 +15,7 @@ from oracle.sampling import filtered_probs
 from oracle.verify import commit_request, greedy_decode, prefill_request, verify_request, verify_tree_request
 from paper_2607_17299_amd import synth
 from paper_2607_17299_amd.drafter import SuffixDrafter
-from parity import compare_request, compare_tree_request, shared_units
+from parity import NEAR_TIE, compare_request, compare_tree_request, shared_units
 
 pytestmark = pytest.mark.gpu
 CFG = synth.TINY
@@ -189,7 +189,7 @@ def test_prefill_matches_oracle(tiny):
     for b in range(len(ctxs)):
         if gnext[b] != onext[b]:
             gap = np.sort(ologits[b])[-1] - np.sort(ologits[b])[-2]
-            assert gap <= 2 * np.abs(glogits[b] - ologits[b]).max() + 1e-6
+            assert gap < NEAR_TIE and gap <= 2 * np.abs(glogits[b] - ologits[b]).max() + 1e-6, (b, gap)
         for l in range(CFG.n_layers):
             g = pool.gather_kv(b, len(ctxs[b]), l).double().cpu().numpy()
             K, V = kvs[b].get(l)
