@@ -710,8 +710,10 @@ k_attn_rows(AttnArgs a) {
 constexpr int kCombMaxItems = 512;
 template <int RB, int HD>
 __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
-  constexpr int TPR = HD / 4;     // threads per row
-  constexpr int RPW = 256 / TPR;  // rows per workgroup
+  constexpr int TPR = HD / 4;                 // threads per row
+  constexpr int RPW = 256 / TPR;              // rows per workgroup
+  constexpr int PF = 16;                      // partial-O loads issued before the weights are known
+  constexpr int IPL = kCombMaxItems / 64;     // items per lane in the weight pass
   __shared__ float s_w[RPW][kCombMaxItems];
   __shared__ float s_il[RPW];
   const int seg = blockIdx.x, kvh = blockIdx.y, r0 = blockIdx.z * RPW;
@@ -727,26 +729,56 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
   const float* pm = a.pm + ((int64_t)ib * a.n_kv_heads + kvh) * RB + r0;
   const float* pl = a.pl + ((int64_t)ib * a.n_kv_heads + kvh) * RB + r0;
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-  for (int r = w; r < rows; r += 4) {
+  // this thread's output float4: the first PF items' partial O are requested
+  // now, so their loads overlap the weight pass
+  const int r = threadIdx.x / TPR, d4 = (threadIdx.x % TPR) * 4;
+  const bool live = r < rows;
+  const float* po = a.po + (((int64_t)ib * a.n_kv_heads + kvh) * RB + r0 + r) * HD + d4;
+  float4 pre[PF];
+#pragma unroll
+  for (int i = 0; i < PF; ++i)
+    if (live && i < ni) pre[i] = *reinterpret_cast<const float4*>(po + i * is * HD);
+  // weight pass, one wave per row: each lane's items (i = lane + 64 j) are
+  // loaded once, max and sum in ascending item order per lane
+  for (int rr = w; rr < rows; rr += 4) {
+    float vm[IPL], vl[IPL];
+#pragma unroll
+    for (int j = 0; j < IPL; ++j) {
+      const int i = lane + 64 * j;
+      vm[j] = i < ni ? pm[i * is + rr] : -INFINITY;
+      vl[j] = i < ni ? pl[i * is + rr] : 0.f;
+    }
     float mm = -INFINITY;
-    for (int i = lane; i < ni; i += 64) mm = fmaxf(mm, pm[i * is + r]);
+#pragma unroll
+    for (int j = 0; j < IPL; ++j) mm = fmaxf(mm, vm[j]);
     mm = wave_max(mm);
     float l = 0.f;
-    for (int i = lane; i < ni; i += 64) {
-      const float f = exp2f(pm[i * is + r] - mm);
-      s_w[r][i] = f;
-      l += pl[i * is + r] * f;
+#pragma unroll
+    for (int j = 0; j < IPL; ++j) {
+      const int i = lane + 64 * j;
+      if (i < ni) {
+        const float f = exp2f(vm[j] - mm);
+        s_w[rr][i] = f;
+        l += vl[j] * f;
+      }
     }
     l = wave_sum(l);
-    if (lane == 0) s_il[r] = 1.f / l;
+    if (lane == 0) s_il[rr] = 1.f / l;
   }
   __syncthreads();
-  const int r = threadIdx.x / TPR, d4 = (threadIdx.x % TPR) * 4;
-  if (r >= rows) return;
-  const float* po = a.po + (((int64_t)ib * a.n_kv_heads + kvh) * RB + r0 + r) * HD + d4;
+  if (!live) return;
   float4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int i = 0; i < PF; ++i)
+    if (i < ni) {
+      const float f = s_w[r][i];
+      acc.x += pre[i].x * f;
+      acc.y += pre[i].y * f;
+      acc.z += pre[i].z * f;
+      acc.w += pre[i].w * f;
+    }
 #pragma unroll 8
-  for (int i = 0; i < ni; ++i) {
+  for (int i = PF; i < ni; ++i) {
     const float4 v = *reinterpret_cast<const float4*>(po + i * is * HD);
     const float f = s_w[r][i];
     acc.x += v.x * f;

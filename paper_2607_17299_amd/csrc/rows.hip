@@ -59,22 +59,20 @@ __global__ void __launch_bounds__(256) k_embed_norm(const int32_t* tok, const bf
   norm_row(hr, d, g, eps, u + (int64_t)r * d, ss, red);
 }
 
-// Sum of the split-K partials of one float4 run: all loads issued before use.
+// Sum of the split-K partials of one float4 run, in split order: the loads of
+// up to eight splits are issued before the first add, so the split counts the
+// projections use cost one memory round trip.
 __device__ __forceinline__ float4 sum_splits(const float* P, int64_t sstride, int splits, float4 x) {
-  int s = 0;
-  for (; s + 4 <= splits; s += 4) {
-    const float4 a = *reinterpret_cast<const float4*>(P + (s + 0) * sstride);
-    const float4 b = *reinterpret_cast<const float4*>(P + (s + 1) * sstride);
-    const float4 c = *reinterpret_cast<const float4*>(P + (s + 2) * sstride);
-    const float4 d = *reinterpret_cast<const float4*>(P + (s + 3) * sstride);
-    x.x += a.x; x.y += a.y; x.z += a.z; x.w += a.w;
-    x.x += b.x; x.y += b.y; x.z += b.z; x.w += b.w;
-    x.x += c.x; x.y += c.y; x.z += c.z; x.w += c.w;
-    x.x += d.x; x.y += d.y; x.z += d.z; x.w += d.w;
-  }
-  for (; s < splits; ++s) {
-    const float4 a = *reinterpret_cast<const float4*>(P + s * sstride);
-    x.x += a.x; x.y += a.y; x.z += a.z; x.w += a.w;
+  for (int s0 = 0; s0 < splits; s0 += 8) {
+    float4 t[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (s0 + u < splits) t[u] = *reinterpret_cast<const float4*>(P + (s0 + u) * sstride);
+#pragma unroll
+    for (int u = 0; u < 8; ++u)
+      if (s0 + u < splits) {
+        x.x += t[u].x; x.y += t[u].y; x.z += t[u].z; x.w += t[u].w;
+      }
   }
   return x;
 }
@@ -237,13 +235,22 @@ __global__ void __launch_bounds__(1024) k_argmax_accept(const int32_t* ntok, int
     const int64_t row = (int64_t)b * row_stride + i;
     float v = -INFINITY;
     int idx = 0x7fffffff;
-    for (int c = lane; c < n_blocks; c += 64) {
-      const float ov = amax_v[row * n_blocks + c];
-      const int oi = amax_i[row * n_blocks + c];
-      if (ov > v || (ov == v && oi < idx)) {
-        v = ov;
-        idx = oi;
+    // lane-strided blocks in ascending order, 16 loads in flight per batch
+    for (int c0 = 0; c0 < n_blocks; c0 += 64 * 16) {
+      float bv[16];
+      int bi[16];
+#pragma unroll
+      for (int u = 0; u < 16; ++u) {
+        const int c = c0 + u * 64 + lane;
+        bv[u] = c < n_blocks ? amax_v[row * n_blocks + c] : -INFINITY;
+        bi[u] = c < n_blocks ? amax_i[row * n_blocks + c] : 0x7fffffff;
       }
+#pragma unroll
+      for (int u = 0; u < 16; ++u)
+        if (bv[u] > v || (bv[u] == v && bi[u] < idx)) {
+          v = bv[u];
+          idx = bi[u];
+        }
     }
 #pragma unroll
     for (int o = 32; o >= 1; o >>= 1) {
