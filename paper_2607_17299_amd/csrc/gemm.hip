@@ -571,7 +571,8 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
     // two m-blocks (97-192 rows) come with 4-6 tiles each
     if (gemm_mw(g.M) == 2 && epi != EPI_PARTIAL) {
       dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 32), splits, 1);
-      if (epi == EPI_ARGMAX) k_gemm_x2<MT, 0, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
+      if (epi == EPI_ARGMAX && g.kper == 64 * KS) k_gemm_x2<MT, 64, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
+      else if (epi == EPI_ARGMAX) k_gemm_x2<MT, 0, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
       else if (g.kper == 64 * KS) k_gemm_x2<MT, 64, EPI_SWIGLU><<<grid, 512, 0, st>>>(g);
       else k_gemm_x2<MT, 0, EPI_SWIGLU><<<grid, 512, 0, st>>>(g);
       return;
@@ -579,7 +580,8 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   }
   if (epi == EPI_ARGMAX) {
     dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 16), splits, 1);
-    k_gemm<MT, 0, EPI_ARGMAX, 1><<<grid, 256, 0, st>>>(g);
+    if (g.kper == 64 * KS) k_gemm<MT, 64, EPI_ARGMAX, 1><<<grid, 256, 0, st>>>(g);
+    else k_gemm<MT, 0, EPI_ARGMAX, 1><<<grid, 256, 0, st>>>(g);
   } else if (gemm_mw(g.M) == 2) {
     launch_mw<MT, 2>(g, epi, splits, st);
   } else {
