@@ -738,28 +738,38 @@ __global__ void __launch_bounds__(256) k_attn_combine(AttnArgs a) {
 #pragma unroll
   for (int i = 0; i < PF; ++i)
     if (live && i < ni) pre[i] = *reinterpret_cast<const float4*>(po + i * is * HD);
-  // weight pass, one wave per row: each lane's items (i = lane + 64 j) are
-  // loaded once, max and sum in ascending item order per lane
-  for (int rr = w; rr < rows; rr += 4) {
-    float vm[IPL], vl[IPL];
+  // weight pass, one wave per row (rows w, w + 4, ...): each lane's items
+  // (i = lane + 64 j) of all of the wave's rows are loaded first, once; max and
+  // sum in ascending item order per lane
+  constexpr int RPV = RPW / 4;                // rows per wave
+  float vm[RPV][IPL], vl[RPV][IPL];
+#pragma unroll
+  for (int q = 0; q < RPV; ++q) {
+    const int rr = w + 4 * q;
 #pragma unroll
     for (int j = 0; j < IPL; ++j) {
       const int i = lane + 64 * j;
-      vm[j] = i < ni ? pm[i * is + rr] : -INFINITY;
-      vl[j] = i < ni ? pl[i * is + rr] : 0.f;
+      const bool ok = rr < rows && i < ni;
+      vm[q][j] = ok ? pm[i * is + rr] : -INFINITY;
+      vl[q][j] = ok ? pl[i * is + rr] : 0.f;
     }
+  }
+#pragma unroll
+  for (int q = 0; q < RPV; ++q) {
+    const int rr = w + 4 * q;
+    if (rr >= rows) break;
     float mm = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < IPL; ++j) mm = fmaxf(mm, vm[j]);
+    for (int j = 0; j < IPL; ++j) mm = fmaxf(mm, vm[q][j]);
     mm = wave_max(mm);
     float l = 0.f;
 #pragma unroll
     for (int j = 0; j < IPL; ++j) {
       const int i = lane + 64 * j;
       if (i < ni) {
-        const float f = exp2f(vm[j] - mm);
+        const float f = exp2f(vm[q][j] - mm);
         s_w[rr][i] = f;
-        l += vl[j] * f;
+        l += vl[q][j] * f;
       }
     }
     l = wave_sum(l);
