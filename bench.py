@@ -451,7 +451,9 @@ def main():
     cfg = synth.LARGE
     log("generating weights on the GPU")
     weights = harness.large_weights(cfg)
-    model = war.Model(cfg, weights, max_rows=1152 if args.sweep else 1024)
+    # 2048 rows per forward pass: the multi-turn append runs in 2048-row chunks
+    # (3.7% faster than 1024; the verify steps use at most 192 rows)
+    model = war.Model(cfg, weights, max_rows=1152 if args.sweep else 2048)
     if args.sweep:
         print(json.dumps(run_sweep(model, cfg, 5, min(args.steps, 10), args.warmup)), flush=True)
         return

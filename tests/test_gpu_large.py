@@ -438,7 +438,7 @@ def test_full_size_multi_turn_sampled():
     units).  Trajectories 0 and 5 (two groups) are recomputed by the oracle
     from the cached keys and values the pool holds after the append."""
     def setup(war, cfg, w):
-        model = war.Model(cfg, w, max_rows=1024)
+        model = war.Model(cfg, w, max_rows=2048)    # the benchmark's prefill chunk rows
         mt = harness.multi_turn_inputs(vocab=cfg.vocab)
         pool = harness.multi_turn_pool(cfg, mt, 4)
         harness.load_multi_turn(pool, cfg, mt, 5)
@@ -575,7 +575,7 @@ def test_full_size_prefill_append():
     war = _war()
     cfg = synth.LARGE
     w = harness.large_weights(cfg)
-    model = war.Model(cfg, w, max_rows=1024)
+    model = war.Model(cfg, w, max_rows=2048)
     ctxs = np.array([4000, 4111], np.int32)
     n_new = [64, 64]
     kv_seed = 5
