@@ -547,10 +547,13 @@ k_attn_rows(AttnArgs a) {
         }
       }
     };
-    // two blocks in flight (register sets A and B) while one is computed
-    uint4 stA[NPC], stB[NPC];
+    // three register sets: while block i is computed from LDS, blocks i + 1
+    // and i + 2 are in flight, so a block's loads have two block computations
+    // to arrive before it is stored to LDS
+    uint4 stA[NPC], stB[NPC], stC[NPC];
     if (nb > 0) gload(stA, kbeg);
     if (nb > 1) gload(stB, kbeg + 32);
+    if (nb > 2) gload(stC, kbeg + 64);
 
     // queries (B operand of S^T) and row positions of this wave's two tiles
     bf16x8 qf[NRW][KSUB];
@@ -658,21 +661,31 @@ k_attn_rows(AttnArgs a) {
         if (dt % 2 == 1) asm volatile("" ::: "memory");
       }
     };
-    // Block i (keys kbeg + 32 i) is in LDS buffer i % 2 when iteration i
-    // starts; block i + 1 is in flight in one register set, and block i + 2 is
-    // requested into the other, which block i left at the end of iteration i-1.
-    for (int i = 0; i < nb; i += 2) {
-      const int kb = kbeg + 32 * i;
-      if (i + 2 < nb) gload(stA, kb + 64);
-      compute_block(0, kb, i >= nfull);
-      if (i + 1 < nb) lstore(1, stB, kb + 32);
-      __syncthreads();
-      if (i + 1 >= nb) break;
-      if (i + 3 < nb) gload(stB, kb + 96);
-      compute_block(1, kb + 32, i + 1 >= nfull);
-      if (i + 2 < nb) lstore(0, stA, kb + 64);
-      __syncthreads();
+    // Block i (keys kbeg + 32 i) is in LDS buffer i % 2 when step i starts;
+    // blocks i + 1 and i + 2 are in register sets (i + 1) % 3 and (i + 2) % 3.
+    // Step i requests block i + 3 into set i % 3 (block i left it for LDS at
+    // the end of step i - 1), computes block i, and stores block i + 1 into the
+    // other LDS buffer (whose block i - 1 every wave finished before the last
+    // barrier).
+#define ROWS_STEP(I, LD, ST, BUF)                                   \
+    {                                                               \
+      const int ii = i + (I);                                       \
+      if (ii >= nb) break;                                          \
+      const int kb = kbeg + 32 * ii;                                \
+      if (ii + 3 < nb) gload(LD, kb + 96);                          \
+      compute_block(BUF, kb, ii >= nfull);                          \
+      if (ii + 1 < nb) lstore(1 - (BUF), ST, kb + 32);              \
+      __syncthreads();                                              \
     }
+    for (int i = 0; i < nb; i += 6) {
+      ROWS_STEP(0, stA, stB, 0)
+      ROWS_STEP(1, stB, stC, 1)
+      ROWS_STEP(2, stC, stA, 0)
+      ROWS_STEP(3, stA, stB, 1)
+      ROWS_STEP(4, stB, stC, 0)
+      ROWS_STEP(5, stC, stA, 1)
+    }
+#undef ROWS_STEP
 
     int next_it = 0;
     if (tid == 0) next_it = atomicAdd(&a.unit_ctr[cls], 1) * NC + cls;
