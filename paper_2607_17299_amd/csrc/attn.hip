@@ -468,9 +468,10 @@ struct UnitRows {
 // Prefill attention over row blocks of NW * 32 rows (a causal run of a
 // sequence's new tokens; G query heads per token).  Wave w owns rows
 // [32w, 32w + 32): two 16-row tiles, queries in registers.  The NW waves share
-// every 32-key block, which all threads stage through LDS (two buffers, with
-// the next two blocks in flight in registers; K rows and V^T rows padded
-// against bank conflicts; V^T columns past the sequence end zeroed), so a key
+// every 32-key block, which all threads stage through LDS (two buffers; the
+// next three blocks in flight in three register sets, each block requested
+// three blocks before it is computed; K rows and V^T rows padded against bank
+// conflicts; V^T columns past the sequence end zeroed), so a key
 // block is read from memory once per NW * 32 rows instead of once per 48 rows
 // as in k_attn.  Per block and wave: S^T = K Q^T
 // for both row tiles (each K fragment read once from LDS), the online softmax
@@ -547,9 +548,9 @@ k_attn_rows(AttnArgs a) {
         }
       }
     };
-    // three register sets: while block i is computed from LDS, blocks i + 1
-    // and i + 2 are in flight, so a block's loads have two block computations
-    // to arrive before it is stored to LDS
+    // three register sets: while block i is computed from LDS, blocks i + 1 to
+    // i + 3 are in flight, so a block's loads have two block computations to
+    // arrive before it is stored to LDS
     uint4 stA[NPC], stB[NPC], stC[NPC];
     if (nb > 0) gload(stA, kbeg);
     if (nb > 1) gload(stB, kbeg + 32);
