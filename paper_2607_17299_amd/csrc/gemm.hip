@@ -40,7 +40,7 @@
 // SwiGLU epilogue (gate/up, one split) takes the paired [gate; up] groups,
 // wave w of block nb owning gate n-tile 4nb + w and the matching up n-tile,
 // and writes bf16 silu(gate) * up for its 16 columns.  At 97-192 rows the
-// SwiGLU and argmax epilogues run in k_gemm_x2 (below).
+// argmax epilogue runs in k_gemm_x2 and the SwiGLU one in k_gemm_x2c (below).
 #include "kernels.h"
 
 namespace {
@@ -298,7 +298,7 @@ __global__ void __launch_bounds__(256 * MW) __attribute__((amdgpu_waves_per_eu(1
 // m-tiles [h ? ceil(MT/2) : 0, h ? MT : ceil(MT/2)) of its m-half.  Same
 // pipeline as k_gemm.  (Measured against k_gemm's two-group mode: gate/up 5%
 // and the LM head 10% faster at 192 rows; the split-K projections slower, so
-// they keep k_gemm.)
+// they keep k_gemm.  One split of gate/up now runs in k_gemm_x2c instead.)
 template <int MT, int NSTEPS, int EPI>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm_x2(GemmArgs g) {
   constexpr int RT = 2 * MT;                             // m-tiles of the workgroup
@@ -545,6 +545,156 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))
   }
 }
 
+// SwiGLU at 97-192 rows (one split of 64 k-steps), column-quarter waves: wave
+// (kh, cq) owns k-half kh of every step and gate tile cq with its up tile 4 + cq
+// for all 2*MT m-tiles (one A fragment read from LDS feeds two MFMAs), so no
+// two waves load the same weight fragment and every weight byte is used by one
+// workgroup (WNT: non-temporal weight loads).  The two k-halves' sums meet in
+// LDS at the end, each wave writing half of the m-tiles.  Gate/up at 100, 128
+// and 192 rows: 45, 50 and 59 us against 56, 56 and 61 us for k_gemm_x2
+// (weights rotated past the memory-side cache).
+template <int MT, int NSTEPS, bool WNT>
+__global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm_x2c(GemmArgs g) {
+  constexpr int RT = 2 * MT;
+  constexpr int A_CHUNKS = RT * 16 * (KS / 8);
+  constexpr int A_PER = (A_CHUNKS + 511) / 512;
+  constexpr int A_BYTES = RT * 16 * ROWB;
+  constexpr int HALF = RT / 2;                       // m-tiles each k-half wave keeps
+  constexpr int X_BYTES = 4 * 2 * HALF * 2 * 64 * 16;
+  constexpr int S_BYTES = 3 * A_BYTES > X_BYTES ? 3 * A_BYTES : X_BYTES;
+  __shared__ __attribute__((aligned(16))) unsigned char smem[S_BYTES];
+  auto sA = [&](int buf) { return smem + buf * A_BYTES; };
+  const int tid = threadIdx.x, lane = tid & 63, ln = lane & 15, lg = lane >> 4;
+  const int wi = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int kh = wi >> 2, cq = wi & 3;
+  const int mblocks = (g.M + RT * 16 - 1) / (RT * 16);
+  const int NB = g.N / 128;
+  const int full = (NB / 8) * 8 * mblocks;
+  int nb, mb;
+  if ((int)blockIdx.x < full) {
+    const int r = blockIdx.x % (8 * mblocks);
+    nb = (blockIdx.x / (8 * mblocks)) * 8 + (r & 7);
+    mb = r >> 3;
+  } else {
+    const int r = blockIdx.x - full;
+    nb = (NB / 8) * 8 + r / mblocks;
+    mb = r % mblocks;
+  }
+  const int m0 = mb * RT * 16;
+  const int kb = 0;
+  const int nsteps = NSTEPS;
+  const int tb = nb * 4;
+  const bf16_t* Wb = g.Wp + (int64_t)nb * (8 * KS * 16);
+  const int NG = g.N / 128;
+  const __amdgpu_buffer_rsrc_t wres =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(Wb), 0, 0x7fffffff, 0x00020000);
+  const __amdgpu_buffer_rsrc_t ares =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(g.A), 0, 0x7fffffff, 0x00020000);
+  const int64_t sstride = (int64_t)NG * (KS * 256);
+  const int wg0 = (cq * 2 + kh) * 1024 + lane * 16, wu0 = ((4 + cq) * 2 + kh) * 1024 + lane * 16;
+  int av[A_PER];
+  int aoff[A_PER];
+#pragma unroll
+  for (int i = 0; i < A_PER; ++i) {
+    const int c = min(tid + 512 * i, A_CHUNKS - 1);
+    const int r = c >> 3, q = c & 7;
+    const int gm = m0 + r;
+    aoff[i] = r * ROWB + q * 16;
+    const int src = gm < g.M ? (g.a_rows ? g.a_rows[gm] : gm) : (g.a_rows ? g.a_rows[0] : 0);
+    av[i] = (src * g.lda + kb + q * 8) * 2;
+  }
+  auto bload = [](__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+  };
+  auto bload_w = [](__amdgpu_buffer_rsrc_t r, int voff, int soff) {  // cache policy 2: non-temporal
+    return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, WNT ? 2 : 0));
+  };
+  auto load_w = [&](uint4* wr, int s) {
+    const int so = (int)(s * sstride);
+    wr[0] = bload_w(wres, wg0, so);
+    wr[1] = bload_w(wres, wu0, so);
+  };
+  auto load_a = [&](uint4* ar, int s) {
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i) ar[i] = bload(ares, av[i], s * KS * 2);
+  };
+  auto store_a = [&](const uint4* ar, int buf) {
+#pragma unroll
+    for (int i = 0; i < A_PER; ++i)
+      if (A_CHUNKS % 512 == 0 || tid + 512 * i < A_CHUNKS)
+        *reinterpret_cast<uint4*>(sA(buf) + aoff[i]) = ar[i];
+  };
+  f32x4 acc[RT][2];
+#pragma unroll
+  for (int mt = 0; mt < RT; ++mt) acc[mt][0] = acc[mt][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto compute = [&](const uint4* wr, int buf) {
+    const bf16x8 b0 = as_bf16x8(wr[0]), b1 = as_bf16x8(wr[1]);
+#pragma unroll
+    for (int mt = 0; mt < RT; ++mt) {
+      const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(sA(buf) + (mt * 16 + ln) * ROWB + lg * 32 + kh * 16));
+      acc[mt][0] = mfma16(a, b0, acc[mt][0]);
+      acc[mt][1] = mfma16(a, b1, acc[mt][1]);
+    }
+  };
+  uint4 wA[2], wB[2], wC[2];
+  uint4 aA[A_PER], aB[A_PER], aC[A_PER];
+  if (nsteps > 0) { load_a(aA, 0); load_w(wA, 0); }
+  if (nsteps > 1) { load_a(aB, 1); load_w(wB, 1); }
+  if (nsteps > 2) { load_a(aC, 2); load_w(wC, 2); }
+  __builtin_amdgcn_sched_barrier(0);
+  if (nsteps > 0) store_a(aA, 0);
+  __syncthreads();
+#define GEMM_STEP(S, AL, AS, WR_, B)                   \
+  if ((S) < nsteps) {                                  \
+    if ((S) + 3 < nsteps) load_a(AL, (S) + 3);         \
+    __builtin_amdgcn_sched_barrier(0);                 \
+    compute(WR_, B);                                   \
+    if ((S) + 3 < nsteps) load_w(WR_, (S) + 3);        \
+    __builtin_amdgcn_sched_barrier(0);                 \
+    if ((S) + 1 < nsteps) store_a(AS, ((B) + 1) % 3);  \
+    __syncthreads();                                   \
+  }
+#pragma unroll
+  for (int s = 0; s < NSTEPS; s += 3) {
+    GEMM_STEP(s, aA, aB, wA, 0)
+    GEMM_STEP(s + 1, aB, aC, wB, 1)
+    GEMM_STEP(s + 2, aC, aA, wC, 2)
+  }
+#undef GEMM_STEP
+  // k-half sums: the kh = 0 wave keeps m-tiles [0, HALF), the kh = 1 wave the rest
+  // (compile-time tile indices in both branches: acc stays in registers)
+  f32x4* xs = reinterpret_cast<f32x4*>(smem);
+  auto xidx = [&](int k, int q, int n) { return (((cq * 2 + k) * HALF + q) * 2 + n) * 64 + lane; };
+  if (kh == 0) {
+#pragma unroll
+    for (int q = 0; q < HALF; ++q)
+#pragma unroll
+      for (int n = 0; n < 2; ++n) xs[xidx(0, q, n)] = acc[HALF + q][n];
+  } else {
+#pragma unroll
+    for (int q = 0; q < HALF; ++q)
+#pragma unroll
+      for (int n = 0; n < 2; ++n) xs[xidx(1, q, n)] = acc[q][n];
+  }
+  __syncthreads();
+  auto out_tile = [&](int t, f32x4 gsum, f32x4 usum) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + t * 16 + lg * 4 + i;
+      const float a = gsum[i];
+      if (m < g.M) g.out[(int64_t)m * g.ld_out + (tb + cq) * 16 + ln] = f2bf(a / (1.f + expf(-a)) * usum[i]);
+    }
+  };
+  if (kh == 0) {
+#pragma unroll
+    for (int q = 0; q < HALF; ++q) out_tile(q, acc[q][0] + xs[xidx(1, q, 0)], acc[q][1] + xs[xidx(1, q, 1)]);
+  } else {
+#pragma unroll
+    for (int q = 0; q < HALF; ++q)
+      out_tile(HALF + q, acc[HALF + q][0] + xs[xidx(0, q, 0)], acc[HALF + q][1] + xs[xidx(0, q, 1)]);
+  }
+}
+
 template <int MT, int MW, bool WNT>
 void launch_mw(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 16 * MW), splits, 1);
@@ -581,6 +731,7 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
       dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 32), splits, 1);
       if (epi == EPI_ARGMAX && g.kper == 64 * KS) k_gemm_x2<MT, 64, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
       else if (epi == EPI_ARGMAX) k_gemm_x2<MT, 0, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
+      else if (g.kper == 64 * KS && g.M <= MT * 32) k_gemm_x2c<MT, 64, true><<<grid, 512, 0, st>>>(g);
       else if (g.kper == 64 * KS) k_gemm_x2<MT, 64, EPI_SWIGLU><<<grid, 512, 0, st>>>(g);
       else k_gemm_x2<MT, 0, EPI_SWIGLU><<<grid, 512, 0, st>>>(g);
       return;
