@@ -40,7 +40,8 @@
 // SwiGLU epilogue (gate/up, one split) takes the paired [gate; up] groups,
 // wave w of block nb owning gate n-tile 4nb + w and the matching up n-tile,
 // and writes bf16 silu(gate) * up for its 16 columns.  At 97-192 rows the
-// argmax epilogue runs in k_gemm_x2 and the SwiGLU one in k_gemm_x2c (below).
+// argmax epilogue runs in k_gemm_x2, and SwiGLU and the partial sums of
+// splits of 8-64 k-steps in k_gemm_x2c (below).
 #include "kernels.h"
 
 namespace {
@@ -298,7 +299,8 @@ __global__ void __launch_bounds__(256 * MW) __attribute__((amdgpu_waves_per_eu(1
 // m-tiles [h ? ceil(MT/2) : 0, h ? MT : ceil(MT/2)) of its m-half.  Same
 // pipeline as k_gemm.  (Measured against k_gemm's two-group mode: gate/up 5%
 // and the LM head 10% faster at 192 rows; the split-K projections slower, so
-// they keep k_gemm.  One split of gate/up now runs in k_gemm_x2c instead.)
+// they kept k_gemm.  Gate/up and the split-K projections now run in
+// k_gemm_x2c instead.)
 template <int MT, int NSTEPS, int EPI>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm_x2(GemmArgs g) {
   constexpr int RT = 2 * MT;                             // m-tiles of the workgroup
@@ -545,16 +547,19 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))
   }
 }
 
-// SwiGLU at 97-192 rows (one split of 64 k-steps), column-quarter waves: wave
-// (kh, cq) owns k-half kh of every step and gate tile cq with its up tile 4 + cq
-// for all 2*MT m-tiles (one A fragment read from LDS feeds two MFMAs), so no
+// SwiGLU (one split of 64 k-steps) and split-K partial sums at 97-192 rows,
+// column-quarter waves: wave (kh, cq) owns k-half kh of every step and two
+// n-tiles (gate tile cq with its up tile 4 + cq, or tiles 2cq, 2cq + 1) for
+// all 2*MT m-tiles (one A fragment read from LDS feeds two MFMAs), so no
 // two waves load the same weight fragment and every weight byte is used by one
 // workgroup (WNT: non-temporal weight loads).  The two k-halves' sums meet in
 // LDS at the end, each wave writing half of the m-tiles.  Gate/up at 100, 128
-// and 192 rows: 45, 50 and 59 us against 56, 56 and 61 us for k_gemm_x2
-// (weights rotated past the memory-side cache).
-template <int MT, int NSTEPS, bool WNT>
+// and 192 rows: 45, 50 and 59 us against 56, 56 and 61 us for k_gemm_x2; at
+// 192 rows qkv 21.8 -> 20.7 us, o 16.4 -> 15.2, down 35.8 -> 32.1 against
+// k_gemm's two-group mode (weights rotated past the memory-side cache).
+template <int MT, int NSTEPS, int EPI, bool WNT>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm_x2c(GemmArgs g) {
+  static_assert(EPI == EPI_SWIGLU || EPI == EPI_PARTIAL, "SwiGLU or partial sums");
   constexpr int RT = 2 * MT;
   constexpr int A_CHUNKS = RT * 16 * (KS / 8);
   constexpr int A_PER = (A_CHUNKS + 511) / 512;
@@ -581,7 +586,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))
     mb = r % mblocks;
   }
   const int m0 = mb * RT * 16;
-  const int kb = 0;
+  const int split = blockIdx.y;
+  const int kb = split * g.kper;
+  const int s0 = kb / KS;
   const int nsteps = NSTEPS;
   const int tb = nb * 4;
   const bf16_t* Wb = g.Wp + (int64_t)nb * (8 * KS * 16);
@@ -591,7 +598,9 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))
   const __amdgpu_buffer_rsrc_t ares =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(g.A), 0, 0x7fffffff, 0x00020000);
   const int64_t sstride = (int64_t)NG * (KS * 256);
-  const int wg0 = (cq * 2 + kh) * 1024 + lane * 16, wu0 = ((4 + cq) * 2 + kh) * 1024 + lane * 16;
+  // the wave's two tiles: SwiGLU gate tile cq and up tile 4 + cq, else tiles 2cq, 2cq + 1
+  const int t0 = EPI == EPI_SWIGLU ? cq : 2 * cq, t1 = EPI == EPI_SWIGLU ? 4 + cq : 2 * cq + 1;
+  const int wg0 = (t0 * 2 + kh) * 1024 + lane * 16, wu0 = (t1 * 2 + kh) * 1024 + lane * 16;
   int av[A_PER];
   int aoff[A_PER];
 #pragma unroll
@@ -610,7 +619,7 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))
     return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, WNT ? 2 : 0));
   };
   auto load_w = [&](uint4* wr, int s) {
-    const int so = (int)(s * sstride);
+    const int so = (int)((s0 + s) * sstride);
     wr[0] = bload_w(wres, wg0, so);
     wr[1] = bload_w(wres, wu0, so);
   };
@@ -681,8 +690,15 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int m = m0 + t * 16 + lg * 4 + i;
-      const float a = gsum[i];
-      if (m < g.M) g.out[(int64_t)m * g.ld_out + (tb + cq) * 16 + ln] = f2bf(a / (1.f + expf(-a)) * usum[i]);
+      if (m >= g.M) continue;
+      if constexpr (EPI == EPI_SWIGLU) {
+        const float a = gsum[i];
+        g.out[(int64_t)m * g.ld_out + (tb + cq) * 16 + ln] = f2bf(a / (1.f + expf(-a)) * usum[i]);
+      } else {
+        float* pr = g.P + ((int64_t)split * g.M + m) * g.N + nb * 128 + ln;
+        pr[t0 * 16] = gsum[i];
+        pr[t1 * 16] = usum[i];
+      }
     }
   };
   if (kh == 0) {
@@ -731,7 +747,7 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
       dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 32), splits, 1);
       if (epi == EPI_ARGMAX && g.kper == 64 * KS) k_gemm_x2<MT, 64, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
       else if (epi == EPI_ARGMAX) k_gemm_x2<MT, 0, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
-      else if (g.kper == 64 * KS && g.M <= MT * 32) k_gemm_x2c<MT, 64, true><<<grid, 512, 0, st>>>(g);
+      else if (g.kper == 64 * KS && g.M <= MT * 32) k_gemm_x2c<MT, 64, EPI_SWIGLU, true><<<grid, 512, 0, st>>>(g);
       else if (g.kper == 64 * KS) k_gemm_x2<MT, 64, EPI_SWIGLU><<<grid, 512, 0, st>>>(g);
       else k_gemm_x2<MT, 0, EPI_SWIGLU><<<grid, 512, 0, st>>>(g);
       return;
@@ -746,6 +762,16 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
     else if (g.kper == 64 * KS) k_gemm<MT, 64, EPI_ARGMAX, 1><<<grid, 256, 0, st>>>(g);
     else k_gemm<MT, 0, EPI_ARGMAX, 1><<<grid, 256, 0, st>>>(g);
   } else if (gemm_mw(g.M) == 2) {
+    if constexpr (MT >= 4) {
+      const int steps = g.kper / KS;
+      const bool exact = (int64_t)g.kper * splits == g.K;
+      dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 32), splits, 1);
+      if (exact && steps == 8) { k_gemm_x2c<MT, 8, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+      if (exact && steps == 16) { k_gemm_x2c<MT, 16, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+      if (exact && steps == 32) { k_gemm_x2c<MT, 32, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+      if (exact && steps == 48) { k_gemm_x2c<MT, 48, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+      if (exact && steps == 64) { k_gemm_x2c<MT, 64, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+    }
     launch_mw<MT, 2, false>(g, epi, splits, st);
   } else if (single) {
     launch_mw<MT, 1, true>(g, epi, splits, st);
