@@ -299,8 +299,8 @@ __global__ void __launch_bounds__(256 * MW) __attribute__((amdgpu_waves_per_eu(1
 // m-tiles [h ? ceil(MT/2) : 0, h ? MT : ceil(MT/2)) of its m-half.  Same
 // pipeline as k_gemm.  (Measured against k_gemm's two-group mode: gate/up 5%
 // and the LM head 10% faster at 192 rows; the split-K projections slower, so
-// they kept k_gemm.  Gate/up and the split-K projections now run in
-// k_gemm_x2c instead.)
+// they kept k_gemm.  Gate/up over 64 k-steps and the split-K projections now
+// run in k_gemm_x2c; this kernel keeps the LM head and gate/up over other K.)
 template <int MT, int NSTEPS, int EPI>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm_x2(GemmArgs g) {
   constexpr int RT = 2 * MT;                             // m-tiles of the workgroup
@@ -747,8 +747,7 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
       dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 32), splits, 1);
       if (epi == EPI_ARGMAX && g.kper == 64 * KS) k_gemm_x2<MT, 64, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
       else if (epi == EPI_ARGMAX) k_gemm_x2<MT, 0, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
-      else if (g.kper == 64 * KS && g.M <= MT * 32) k_gemm_x2c<MT, 64, EPI_SWIGLU, true><<<grid, 512, 0, st>>>(g);
-      else if (g.kper == 64 * KS) k_gemm_x2<MT, 64, EPI_SWIGLU><<<grid, 512, 0, st>>>(g);
+      else if (g.kper == 64 * KS) k_gemm_x2c<MT, 64, EPI_SWIGLU, true><<<grid, 512, 0, st>>>(g);
       else k_gemm_x2<MT, 0, EPI_SWIGLU><<<grid, 512, 0, st>>>(g);
       return;
     }
