@@ -87,6 +87,10 @@ def _check_step(env, st, report, tag):
     # 108 rows: two 64-row m-blocks, taken by one GEMM workgroup
     (8, [8, 3, 0, 8, 1, 6, 2, 8, 0, 5, 8, 4],
      [300, 1200, 77, 2100, 640, 90, 1500, 33, 1025, 400, 260, 700]),
+    # 50 rows: the projections in one 64-row tile (14 padding rows)
+    (4, [4, 0, 2, 4, 1, 3, 4, 0, 4, 2], [500, 17, 1600, 48, 900, 2049, 64, 311, 1200, 95]),
+    # 150 rows: two 80-row m-blocks in one workgroup (10 padding rows)
+    (2, [b % 3 for b in range(50)], [16 + (37 * b) % 300 for b in range(50)]),
 ])
 def test_reduced_depth_verify_matches_oracle(large2, k, lens, ctxs):
     cfg = large2["cfg"]
