@@ -547,25 +547,25 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))
   }
 }
 
-// SwiGLU (one split of 64 k-steps) and split-K partial sums at 97-192 rows,
+// SwiGLU (one split of 64 k-steps) and split-K partial sums at 33-192 rows,
 // column-quarter waves: wave (kh, cq) owns k-half kh of every step and two
 // n-tiles (gate tile cq with its up tile 4 + cq, or tiles 2cq, 2cq + 1) for
-// all 2*MT m-tiles (one A fragment read from LDS feeds two MFMAs), so no
+// all RT m-tiles (one A fragment read from LDS feeds two MFMAs), so no
 // two waves load the same weight fragment and every weight byte is used by one
 // workgroup (WNT: non-temporal weight loads).  The two k-halves' sums meet in
-// LDS at the end, each wave writing half of the m-tiles.  Gate/up at 100, 128
+// LDS at the end, the kh = 0 waves writing the first ceil(RT/2) m-tiles and
+// the kh = 1 waves the rest.  Gate/up at 100, 128
 // and 192 rows: 45, 50 and 59 us against 56, 56 and 61 us for k_gemm_x2; at
 // 192 rows qkv 21.8 -> 20.7 us, o 16.4 -> 15.2, down 35.8 -> 32.1 against
 // k_gemm's two-group mode (weights rotated past the memory-side cache).
-template <int MT, int NSTEPS, int EPI, bool WNT>
+template <int RT, int NSTEPS, int EPI, bool WNT>
 __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))) k_gemm_x2c(GemmArgs g) {
   static_assert(EPI == EPI_SWIGLU || EPI == EPI_PARTIAL, "SwiGLU or partial sums");
-  constexpr int RT = 2 * MT;
   constexpr int A_CHUNKS = RT * 16 * (KS / 8);
   constexpr int A_PER = (A_CHUNKS + 511) / 512;
   constexpr int A_BYTES = RT * 16 * ROWB;
-  constexpr int HALF = RT / 2;                       // m-tiles each k-half wave keeps
-  constexpr int X_BYTES = 4 * 2 * HALF * 2 * 64 * 16;
+  constexpr int LO = (RT + 1) / 2, HI = RT - LO;     // m-tiles the k-half 0 / 1 waves keep
+  constexpr int X_BYTES = 4 * 2 * LO * 2 * 64 * 16;
   constexpr int S_BYTES = 3 * A_BYTES > X_BYTES ? 3 * A_BYTES : X_BYTES;
   __shared__ __attribute__((aligned(16))) unsigned char smem[S_BYTES];
   auto sA = [&](int buf) { return smem + buf * A_BYTES; };
@@ -670,18 +670,18 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))
     GEMM_STEP(s + 2, aC, aA, wC, 2)
   }
 #undef GEMM_STEP
-  // k-half sums: the kh = 0 wave keeps m-tiles [0, HALF), the kh = 1 wave the rest
+  // k-half sums: the kh = 0 wave keeps m-tiles [0, LO), the kh = 1 wave the rest
   // (compile-time tile indices in both branches: acc stays in registers)
   f32x4* xs = reinterpret_cast<f32x4*>(smem);
-  auto xidx = [&](int k, int q, int n) { return (((cq * 2 + k) * HALF + q) * 2 + n) * 64 + lane; };
+  auto xidx = [&](int k, int q, int n) { return (((cq * 2 + k) * LO + q) * 2 + n) * 64 + lane; };
   if (kh == 0) {
 #pragma unroll
-    for (int q = 0; q < HALF; ++q)
+    for (int q = 0; q < HI; ++q)
 #pragma unroll
-      for (int n = 0; n < 2; ++n) xs[xidx(0, q, n)] = acc[HALF + q][n];
+      for (int n = 0; n < 2; ++n) xs[xidx(0, q, n)] = acc[LO + q][n];
   } else {
 #pragma unroll
-    for (int q = 0; q < HALF; ++q)
+    for (int q = 0; q < LO; ++q)
 #pragma unroll
       for (int n = 0; n < 2; ++n) xs[xidx(1, q, n)] = acc[q][n];
   }
@@ -703,11 +703,11 @@ __global__ void __launch_bounds__(512) __attribute__((amdgpu_waves_per_eu(1, 2))
   };
   if (kh == 0) {
 #pragma unroll
-    for (int q = 0; q < HALF; ++q) out_tile(q, acc[q][0] + xs[xidx(1, q, 0)], acc[q][1] + xs[xidx(1, q, 1)]);
+    for (int q = 0; q < LO; ++q) out_tile(q, acc[q][0] + xs[xidx(1, q, 0)], acc[q][1] + xs[xidx(1, q, 1)]);
   } else {
 #pragma unroll
-    for (int q = 0; q < HALF; ++q)
-      out_tile(HALF + q, acc[HALF + q][0] + xs[xidx(0, q, 0)], acc[HALF + q][1] + xs[xidx(0, q, 1)]);
+    for (int q = 0; q < HI; ++q)
+      out_tile(LO + q, acc[LO + q][0] + xs[xidx(0, q, 0)], acc[LO + q][1] + xs[xidx(0, q, 1)]);
   }
 }
 
@@ -747,7 +747,7 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
       dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 32), splits, 1);
       if (epi == EPI_ARGMAX && g.kper == 64 * KS) k_gemm_x2<MT, 64, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
       else if (epi == EPI_ARGMAX) k_gemm_x2<MT, 0, EPI_ARGMAX><<<grid, 512, 0, st>>>(g);
-      else if (g.kper == 64 * KS) k_gemm_x2c<MT, 64, EPI_SWIGLU, true><<<grid, 512, 0, st>>>(g);
+      else if (g.kper == 64 * KS) k_gemm_x2c<2 * MT, 64, EPI_SWIGLU, true><<<grid, 512, 0, st>>>(g);
       else k_gemm_x2<MT, 0, EPI_SWIGLU><<<grid, 512, 0, st>>>(g);
       return;
     }
@@ -765,11 +765,11 @@ void launch_mt(const GemmArgs& g, int epi, int splits, hipStream_t st) {
       const int steps = g.kper / KS;
       const bool exact = (int64_t)g.kper * splits == g.K;
       dim3 grid((g.N / 128) * cdiv_i(g.M, MT * 32), splits, 1);
-      if (exact && steps == 8) { k_gemm_x2c<MT, 8, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
-      if (exact && steps == 16) { k_gemm_x2c<MT, 16, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
-      if (exact && steps == 32) { k_gemm_x2c<MT, 32, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
-      if (exact && steps == 48) { k_gemm_x2c<MT, 48, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
-      if (exact && steps == 64) { k_gemm_x2c<MT, 64, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+      if (exact && steps == 8) { k_gemm_x2c<2 * MT, 8, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+      if (exact && steps == 16) { k_gemm_x2c<2 * MT, 16, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+      if (exact && steps == 32) { k_gemm_x2c<2 * MT, 32, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+      if (exact && steps == 48) { k_gemm_x2c<2 * MT, 48, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
+      if (exact && steps == 64) { k_gemm_x2c<2 * MT, 64, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g); return; }
     }
     launch_mw<MT, 2, false>(g, epi, splits, st);
   } else if (single) {
@@ -821,28 +821,45 @@ int gemm_mw(int M) { return cdiv_i(M, 16 * gemm_mt(M)) == 2 ? 2 : 1; }
 // workgroups per 128-column block and split
 int gemm_mblock_groups(int M) { return cdiv_i(M, 16 * gemm_mt(M) * gemm_mw(M)); }
 
-// 33-64 rows: the column-quarter kernel with two m-tiles per k-half wave (its
-// 64-row tile then holds the rows exactly), for SwiGLU and exact splits of
-// 8-64 k-steps.  At 64 rows qkv 13.1 -> 12.1 us, o 10.3 -> 9.5, gate/up 38.4
-// -> 37.8, down 22.8 -> 22.1 (weights rotated); at 65-96 rows its 96-row tile
-// wastes a quarter of the rows and k_gemm is as fast or faster.
+// 33-64 rows: the column-quarter kernel with four m-tiles (its 64-row tile
+// then holds the rows exactly), for SwiGLU and exact splits of 8-64 k-steps.
+// At 64 rows qkv 13.1 -> 12.1 us, o 10.3 -> 9.5, gate/up 38.4 -> 37.8, down
+// 22.8 -> 22.1 (weights rotated).
 bool launch_x2c_64(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   const int steps = g.kper / KS;
   if ((int64_t)g.kper * splits != g.K) return false;
   dim3 grid((g.N / 128) * cdiv_i(g.M, 64), splits, 1);
   if (epi == EPI_SWIGLU) {
     if (steps != 64) return false;
-    k_gemm_x2c<2, 64, EPI_SWIGLU, true><<<grid, 512, 0, st>>>(g);
+    k_gemm_x2c<4, 64, EPI_SWIGLU, true><<<grid, 512, 0, st>>>(g);
   } else if (steps == 8) {
-    k_gemm_x2c<2, 8, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
+    k_gemm_x2c<4, 8, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
   } else if (steps == 16) {
-    k_gemm_x2c<2, 16, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
+    k_gemm_x2c<4, 16, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
   } else if (steps == 32) {
-    k_gemm_x2c<2, 32, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
+    k_gemm_x2c<4, 32, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
   } else if (steps == 48) {
-    k_gemm_x2c<2, 48, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
+    k_gemm_x2c<4, 48, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
   } else if (steps == 64) {
-    k_gemm_x2c<2, 64, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
+    k_gemm_x2c<4, 64, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
+  } else {
+    return false;
+  }
+  return true;
+}
+
+// 65-80 rows: the short split-K projections (splits of 8 and 16 k-steps: qkv
+// and o) take the column-quarter kernel with five m-tiles; at 72 rows qkv and
+// o run 3-4% faster than in k_gemm, while gate/up and the 32-step down
+// projection run 1-4% slower and stay there (weights rotated).
+bool launch_x2c_80(const GemmArgs& g, int epi, int splits, hipStream_t st) {
+  const int steps = g.kper / KS;
+  if (epi != EPI_PARTIAL || (int64_t)g.kper * splits != g.K) return false;
+  dim3 grid((g.N / 128) * cdiv_i(g.M, 80), splits, 1);
+  if (steps == 8) {
+    k_gemm_x2c<5, 8, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
+  } else if (steps == 16) {
+    k_gemm_x2c<5, 16, EPI_PARTIAL, true><<<grid, 512, 0, st>>>(g);
   } else {
     return false;
   }
@@ -851,6 +868,7 @@ bool launch_x2c_64(const GemmArgs& g, int epi, int splits, hipStream_t st) {
 
 void launch_gemm(const GemmArgs& g, int epi, int splits, hipStream_t st) {
   if (g.M > 32 && g.M <= 64 && epi != EPI_ARGMAX && launch_x2c_64(g, epi, splits, st)) return;
+  if (g.M > 64 && g.M <= 80 && launch_x2c_80(g, epi, splits, st)) return;
   switch (gemm_mt(g.M)) {
     case 1: launch_mt<1>(g, epi, splits, st); break;
     case 2: launch_mt<2>(g, epi, splits, st); break;

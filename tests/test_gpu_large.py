@@ -89,6 +89,9 @@ def _check_step(env, st, report, tag):
      [300, 1200, 77, 2100, 640, 90, 1500, 33, 1025, 400, 260, 700]),
     # 50 rows: the projections in one 64-row tile (14 padding rows)
     (4, [4, 0, 2, 4, 1, 3, 4, 0, 4, 2], [500, 17, 1600, 48, 900, 2049, 64, 311, 1200, 95]),
+    # 72 and 80 rows: qkv and o in one 80-row column-quarter tile, gate/up and down in k_gemm
+    (8, [8, 0, 3, 8, 5, 1, 8, 2], [900, 64, 1500, 33, 2100, 400, 17, 1025]),
+    (4, [b % 5 for b in range(16)], [40 + (53 * b) % 900 for b in range(16)]),
     # 150 rows: two 80-row m-blocks in one workgroup (10 padding rows)
     (2, [b % 3 for b in range(50)], [16 + (37 * b) % 300 for b in range(50)]),
 ])
