@@ -41,7 +41,8 @@
 // wave w of block nb owning gate n-tile 4nb + w and the matching up n-tile,
 // and writes bf16 silu(gate) * up for its 16 columns.  At 97-192 rows the
 // argmax epilogue runs in k_gemm_x2, and SwiGLU and the partial sums of
-// splits of 8-64 k-steps in k_gemm_x2c (below).
+// splits of 8-64 k-steps in k_gemm_x2c (below); k_gemm_x2c also takes 33-64
+// rows (SwiGLU and partial sums) and the 8- and 16-step splits at 65-80 rows.
 #include "kernels.h"
 
 namespace {
