@@ -25,6 +25,7 @@ from typing import Dict, List
 import numpy as np
 
 from oracle.accept import argmax_lowest, top2_gap
+from oracle.sampling import filtered_probs
 
 LOGIT_TOL = 5e-2
 NEAR_TIE = 0.1
@@ -132,3 +133,24 @@ def compare_tree_request(o: Dict, g_logits: np.ndarray, tokens, parents, g_accep
         return True
     report.append(f"{tag}: path {list(g_path)} vs oracle {o['path']} at a near-tie")
     return list(g_path) == o["path"]
+
+
+def near_sampled_decision(logits, T, top_k, err, margins) -> bool:
+    """True if a logit error of `err` could change one of the sampled decisions
+    on the oracle's path: some margin (in probability) is below the bound
+    exp(2 err / T) - 1 on how far the error moves a probability or a cumulative
+    sum, plus twice the probability mass of the kept tokens within 2 err of the
+    top_k boundary (the kept set itself may change there)."""
+    delta = np.expm1(2 * err / T) + 1e-5
+    for i in range(len(margins)):
+        z = logits[min(i, len(logits) - 1)]
+        zs = np.sort(z)[::-1]
+        if top_k < z.size:
+            kth = zs[top_k - 1]
+            p = filtered_probs(z, T, top_k)
+            delta_i = delta + 2 * p[np.abs(z - kth) < 2 * err].sum()
+        else:
+            delta_i = delta
+        if margins[i] < delta_i:
+            return True
+    return False

@@ -17,6 +17,8 @@ the oracle reads the very same keys and values; after the multi-turn append
 the oracle reads the cached keys and values back from the pool (the append's
 own parity is checked at reduced depth).
 """
+import copy
+
 import numpy as np
 import pytest
 import torch
@@ -24,7 +26,8 @@ import torch
 from oracle.decoder import RequestKV, Weights, forward_block
 from oracle.verify import greedy_decode, prefill_request, verify_request, verify_tree_request
 from paper_2607_17299_amd import harness, synth
-from parity import NEAR_TIE, compare_request, compare_tree_request, fp32_drift_tol, shared_units
+from parity import (NEAR_TIE, compare_request, compare_tree_request, fp32_drift_tol,
+                    near_sampled_decision, shared_units)
 
 pytestmark = pytest.mark.gpu
 KV_SEED = 9
@@ -137,6 +140,66 @@ def test_rows_do_not_depend_on_later_drafts(large2, k):
         rows = k if b == 1 else k + 1   # request 1's last row saw the changed token
         np.testing.assert_array_equal(out[0][b, :rows], out[1][b, :rows], err_msg=f"k={k} req {b}")
     assert not np.array_equal(out[0][1, k], out[1][1, k])
+
+
+@pytest.mark.parametrize("T,top_k", [(1.0, 200), (0.7, 50)])
+def test_reduced_depth_sampled_matches_oracle(large2, T, top_k):
+    """Sampled verification at full widths (d 4096, vocabulary 151,936; 2
+    layers): ragged drafts, half of them the oracle's greedy continuation, and
+    seeded uniforms.  The GPU's decisions equal the oracle's sampled rule on the
+    oracle's logits with the same uniforms, except where the measured logit
+    error could move a draw (reported), and the committed context lengths
+    follow the GPU's accept lengths."""
+    from oracle.sampling import verify_sampled
+    war, cfg, model, W = large2["war"], large2["cfg"], large2["model"], large2["W"]
+    ctxs = np.array([1500, 33, 2049, 700], np.int32)
+    B, k = len(ctxs), 4
+    rng = np.random.default_rng(int(T * 10) + top_k)
+    last = synth.uniform_tokens(77 + top_k, B, cfg.vocab)
+    pool = harness.make_pool(cfg, ctxs, k + 2)
+    harness.load_contexts(pool, cfg, ctxs, np.arange(B), KV_SEED)
+    kvs = [RequestKV(cfg, [_oracle_kv(cfg, b, int(ctxs[b]))(l) for l in range(cfg.n_layers)]) for b in range(B)]
+    drafts = []
+    for b in range(B):
+        n = int(rng.integers(0, k + 1))
+        if b % 2 == 0:
+            d = greedy_decode(cfg, W, copy.deepcopy(kvs[b]), int(last[b]), n)
+        else:
+            d = [int(x) for x in rng.integers(0, cfg.vocab, n)]
+        drafts.append(d)
+    dt = np.zeros((B, k), np.int32)
+    for b, d in enumerate(drafts):
+        dt[b, : len(d)] = d
+    u = rng.random((B * (k + 1), 2)).astype(np.float32)
+    t = lambda a: torch.as_tensor(np.asarray(a), dtype=torch.int32).to("cuda")
+    seq, ctx = t(np.arange(B)), t(ctxs)
+    acc, nx = t([0] * B), t([0] * B)
+    logits = torch.zeros((B * (k + 1), cfg.vocab), device="cuda")
+    war.verify_step_sampled(model, pool, seq, ctx, t(last), t(dt), t([len(d) for d in drafts]), k,
+                            torch.from_numpy(u).to("cuda"), T, top_k, acc, nx, logits)
+    torch.cuda.synchronize()
+    g_acc, g_nxt = acc.cpu().numpy(), nx.cpu().numpy()
+    glog = logits.cpu().numpy().reshape(B, k + 1, cfg.vocab)
+    report, exact = [], 0
+    for b in range(B):
+        n = len(drafts[b])
+        r = verify_request(cfg, W, kvs[b], int(last[b]), drafts[b])
+        uu = u[b * (k + 1): b * (k + 1) + n + 1].astype(np.float64)
+        rs = verify_sampled(r["logits"], drafts[b], uu[:, 0], uu[:, 1], T, top_k)
+        err = float(np.abs(glog[b, : n + 1] - r["logits"]).max())
+        assert err < 5e-2, (b, err)
+        assert 0 <= g_acc[b] <= n and 0 <= g_nxt[b] < cfg.vocab
+        if (int(g_acc[b]), int(g_nxt[b])) != (rs["accept"], rs["next"]):
+            assert near_sampled_decision(r["logits"], T, top_k, err, rs["margins"]), \
+                (b, (int(g_acc[b]), int(g_nxt[b])), (rs["accept"], rs["next"]), rs["margins"], err)
+            report.append(f"req {b}: near-boundary sample differs")
+        else:
+            exact += 1
+    war.kv_commit(pool, seq, ctx, acc)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ctx.cpu().numpy(), ctxs + g_acc + 1)
+    print(f"\nsampled at full widths T={T} top_k={top_k}: accept {g_acc.tolist()}, {exact} exact, "
+          f"reported {report}")
 
 
 @pytest.mark.parametrize("k", [3, 11])

@@ -11,11 +11,10 @@ import torch
 from oracle.accept import argmax_lowest
 from oracle.decoder import RequestKV, Weights
 from oracle.pages import PagePool
-from oracle.sampling import filtered_probs
 from oracle.verify import commit_request, greedy_decode, prefill_request, verify_request, verify_tree_request
 from paper_2607_17299_amd import synth
 from paper_2607_17299_amd.drafter import SuffixDrafter
-from parity import NEAR_TIE, compare_request, compare_tree_request, shared_units
+from parity import NEAR_TIE, compare_request, compare_tree_request, near_sampled_decision, shared_units
 
 pytestmark = pytest.mark.gpu
 CFG = synth.TINY
@@ -501,27 +500,6 @@ def test_tree_parent_out_of_range_is_flagged(tiny):
     assert path.cpu().tolist()[0] == [1, 2, 3][:a] + [-1] * (3 - a)
 
 
-def _near_decision(logits, T, top_k, err, margins):
-    """True if a logit error of `err` could change one of the sampled decisions
-    on the oracle's path: some margin (in probability) is below the bound
-    exp(2 err / T) - 1 on how far the error moves a probability or a cumulative
-    sum, plus twice the probability mass of the kept tokens within 2 err of the
-    top_k boundary (the kept set itself may change there)."""
-    delta = np.expm1(2 * err / T) + 1e-5
-    for i in range(len(margins)):
-        z = logits[min(i, len(logits) - 1)]
-        zs = np.sort(z)[::-1]
-        if top_k < z.size:
-            kth = zs[top_k - 1]
-            p = filtered_probs(z, T, top_k)
-            delta_i = delta + 2 * p[np.abs(z - kth) < 2 * err].sum()
-        else:
-            delta_i = delta
-        if margins[i] < delta_i:
-            return True
-    return False
-
-
 @pytest.mark.parametrize("T,top_k", [(1.0, 200), (0.7, 50)])
 def test_sampled_verification_matches_oracle(tiny, T, top_k):
     """Three sampled verify steps (k = 4, ragged drafts: the oracle's greedy
@@ -567,7 +545,7 @@ def test_sampled_verification_matches_oracle(tiny, T, top_k):
             err = float(np.abs(glog[b, : n + 1] - r["logits"]).max())
             assert err < 5e-2, err
             if (int(g_acc[b]), int(g_nxt[b])) != (rs["accept"], rs["next"]):
-                assert _near_decision(r["logits"], T, top_k, err, rs["margins"]), \
+                assert near_sampled_decision(r["logits"], T, top_k, err, rs["margins"]), \
                     (step, b, (int(g_acc[b]), int(g_nxt[b])), (rs["accept"], rs["next"]), rs["margins"], err)
                 report.append(f"step {step} req {b}: near-boundary sample differs")
             else:
