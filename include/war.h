@@ -100,8 +100,13 @@ void war_model_destroy(war_model* m);
  *   kv_pages     bf16, n_layers * num_pages * n_kv_heads * 2 * page_size * head_dim
  *                elements.  Page p of layer l, kv-head h starts at element
  *                ((l * num_pages + p) * n_kv_heads + h) * 2 * page_size * head_dim.
- *                It holds the keys as [page_size][head_dim], then the values
- *                transposed as [head_dim][page_size].
+ *                It holds the keys (page_size * head_dim elements, in the
+ *                fragment order below), then the values transposed as
+ *                [head_dim][page_size].  page_size is 16.  Key slot s, dim d
+ *                sits at element ((t * head_dim/32 + d/32) * 8 + s8) * 32 + d%32
+ *                of the key region, with t = (s/4) % 2 and s8 = 4 (s/8) + s%4:
+ *                one 512-byte run per (slot group t, 32-dim step), which is
+ *                what one attention operand load reads.
  *   block_tables int32 [max_seqs][max_pages_per_seq].  Entry [s][j] is the
  *                physical page of sequence s's logical page j, or -1.
  *                Initialised to -1 here.

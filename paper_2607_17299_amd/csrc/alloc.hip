@@ -487,7 +487,7 @@ __global__ void k_kv_load(PoolDev p, KvGeom g, int seq, int layer, int pos0, int
     const int pos = pos0 + tkn;
     const int page = row[pos / p.page_size], slot = pos % p.page_size;
     bf16_t* base = g.kv + g.page_elems(layer, page, kvh, kind);
-    const int64_t o = kind == 0 ? (int64_t)slot * g.head_dim + d : (int64_t)d * p.page_size + slot;
+    const int64_t o = kind == 0 ? key_elem(slot, d, g.head_dim) : (int64_t)d * p.page_size + slot;
     base[o] = src[e];
   }
 }

@@ -10,8 +10,9 @@
 // by the step setup; a persistent grid strides over the items.  Inside an item
 // the 4 waves split the chunk's keys; each wave walks 32-key blocks (two pages):
 //   S^T = K Q^T  -- v_mfma_f32_16x16x32_bf16 with the keys as the M side:
-//                   k-step j covers dims 32j..32j+31, so the 4 lane groups of
-//                   one load read 64 contiguous bytes of each of 16 key rows;
+//                   k-step j covers dims 32j..32j+31, and the keys are
+//                   stored in fragment order (key_elem), so one load of a
+//                   wave reads 512 contiguous bytes from each of two pages;
 //                   key m of tile t is chosen as (m/4)*8 + 4t + m%4 so that
 //                   every lane ends up holding 8 consecutive keys of one row;
 //   online softmax in fp32 (exp2, running max/sum per query row), P split
@@ -71,10 +72,11 @@ k_attn(AttnArgs a) {
   const int P = a.kv.page_size;
   // key row of this lane in S^T tile t (within a 32-key block); tile 1 adds 4
   const int kk0 = (ln >> 2) * 8 + (ln & 3);
-  // Per-lane element offsets inside a page (kind 0 = K [slot][dim], kind 1 =
-  // V^T [dim][slot]): lanes ln < 8 read K rows of the block's first page, the
-  // others its second; lane groups lg < 2 read V^T of the first page.
-  const int koff0 = (kk0 & 15) * HD + lg * 8, koff1 = ((kk0 + 4) & 15) * HD + lg * 8;
+  // Per-lane element offsets inside a page (kind 0 = K in fragment order, see
+  // key_elem; kind 1 = V^T [dim][slot]): lanes ln < 8 read K rows of the
+  // block's first page, the others its second; lane groups lg < 2 read V^T of
+  // the first page.  K of tile t, k-step j is one 512-byte run per page.
+  const int koff0 = key_elem(kk0 & 15, lg * 8, HD), koff1 = key_elem((kk0 + 4) & 15, lg * 8, HD);
   const int voff = P * HD + (lg & 1) * 8 + ln * P;
   const bool k_second = ln >= 8, v_second = lg >= 2;
 
@@ -159,8 +161,8 @@ k_attn(AttnArgs a) {
       const bf16_t* kp = kvb + (int64_t)(k_second ? pg1 : pg0) * pstride;
 #pragma unroll
       for (int j = 0; j < KSUB; ++j) {
-        f.k[0][j] = ntload(kp + koff0 + j * 32);
-        f.k[1][j] = ntload(kp + koff1 + j * 32);
+        f.k[0][j] = ntload(kp + koff0 + j * 256);
+        f.k[1][j] = ntload(kp + koff1 + j * 256);
       }
       const bf16_t* vp = kvb + (int64_t)(v_second ? pg1 : pg0) * pstride + voff;
 #pragma unroll
@@ -529,9 +531,10 @@ k_attn_rows(AttnArgs a) {
 
     // A 32-key block is four regions of 2 HD 16-byte pieces in memory: K and
     // V^T of its two pages.  Piece q of a region sits at q * 8 elements from
-    // the region's start; in LDS, piece q of K page g is key g*16 + q/(HD/8),
-    // dims (q % (HD/8)) * 8, and piece q of V^T page g is dim q/2, keys
-    // g*16 + (q%2)*8.  Thread t moves pieces t, t + NT, ... of the 8 HD.
+    // the region's start; in LDS, piece q of K page g goes to the key and dims
+    // that key_elem places there (rows g*16 + slot), and piece q of V^T page g
+    // is dim q/2, keys g*16 + (q%2)*8.  Thread t moves pieces t, t + NT, ... of
+    // the 8 HD.
     constexpr int NPC = 8 * HD / NT;  // pieces per thread
     static_assert(8 * HD % NT == 0 && NT % (2 * HD) == 0 || (2 * HD) % NT == 0, "piece mapping");
     auto gload = [&](uint4 (&stg)[NPC], int kb) __attribute__((always_inline)) {
@@ -550,7 +553,11 @@ k_attn_rows(AttnArgs a) {
       for (int i = 0; i < NPC; ++i) {
         const int pc = tid + i * NT, reg = pc / (2 * HD), q = pc % (2 * HD);
         if (reg < 2) {
-          *reinterpret_cast<uint4*>(&s_k[buf][((reg & 1) * 16 + q / (HD / 8)) * KST + (q % (HD / 8)) * 8]) = stg[i];
+          // piece q of the page's K in fragment order (key_elem): dims j*32 +
+          // (q%4)*8, slot (s8/4)*8 + t*4 + s8%4 with s8 = (q/4)%8, t*KSUB + j = q/32
+          const int s8 = (q >> 2) & 7, tj = q >> 5, t = tj / KSUB, j = tj % KSUB;
+          const int slot = ((s8 >> 2) << 3) | (t << 2) | (s8 & 3);
+          *reinterpret_cast<uint4*>(&s_k[buf][((reg & 1) * 16 + slot) * KST + j * 32 + (q & 3) * 8]) = stg[i];
         } else {
           uint4 v = stg[i];
           if (kb + 32 > S) v = keep_first(v, min(max(S - (kb + (reg & 1) * 16 + (q & 1) * 8), 0), 8));

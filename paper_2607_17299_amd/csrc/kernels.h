@@ -8,7 +8,10 @@
 // Geometry of the paged KV storage:
 //   element offset of page `page`, layer `layer`, kv-head `kvh`, kind (0 = K, 1 = V^T)
 //   = ((((layer * num_pages + page) * n_kv_heads + kvh) * 2 + kind) * page_size * head_dim
-// K is stored [page_size][head_dim]; V transposed, [head_dim][page_size].
+// V is stored transposed, [head_dim][page_size].  K (page_size = 16) is stored
+// in the order the attention's MFMA fragments read it, so that every K load of
+// a wave reads 512 contiguous bytes of a page: key slot s, dim d sits at
+// key_elem(s, d) (below).
 struct KvGeom {
   bf16_t* kv;
   int64_t num_pages;
@@ -18,6 +21,17 @@ struct KvGeom {
            (int64_t)page_size * head_dim;
   }
 };
+
+// Element offset of key slot s (0..15), dim d in a page's K region.  The slots
+// form two groups of eight, t = (s / 4) % 2 (slots 0-3, 8-11 and 4-7, 12-15:
+// the two 16-key S^T tiles of a 32-key block take one group from each of the
+// block's two pages), and the dims 32-wide k-steps j = d / 32; group t, k-step
+// j is one 512-byte run of eight 64-byte rows (member s8 = 4 (s / 8) + s % 4),
+// which is what one MFMA operand load of a wave reads from the page.
+__host__ __device__ inline int key_elem(int s, int d, int head_dim) {
+  const int t = (s >> 2) & 1, s8 = ((s >> 3) << 2) | (s & 3);
+  return ((t * (head_dim >> 5) + (d >> 5)) * 8 + s8) * 32 + (d & 31);
+}
 
 struct VerifySetupArgs {
   int B, k_max, vocab;

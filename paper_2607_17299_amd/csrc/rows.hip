@@ -201,9 +201,9 @@ __global__ void __launch_bounds__(64) k_qkv_rope(int rows, int splits, const flo
     *reinterpret_cast<uint2*>(qr + j + half) = pack4(b2);
   } else if (act) {
     bf16_t* base = kv.kv + kv.page_elems(layer, page, head, region - 1);
-    if (region == 1) {
-      *reinterpret_cast<uint2*>(base + slot * md.hd + j) = pack4(b1);
-      *reinterpret_cast<uint2*>(base + slot * md.hd + j + half) = pack4(b2);
+    if (region == 1) {  // K in fragment order: dims j..j+3 stay within one 32-dim k-step
+      *reinterpret_cast<uint2*>(base + key_elem(slot, j, md.hd)) = pack4(b1);
+      *reinterpret_cast<uint2*>(base + key_elem(slot, j + half, md.hd)) = pack4(b2);
     } else {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -318,7 +318,7 @@ __global__ void __launch_bounds__(256) k_kv_compact(KvGeom kv, StepMeta meta, co
     const int d = e / D, c = e % D;
     const int sp = ctx + s_src[d];
     const int pg = trow[sp / P], sl = sp % P;
-    s_k[d][c] = kv.kv[kv.page_elems(layer, pg, kvh, 0) + (int64_t)sl * D + c];
+    s_k[d][c] = kv.kv[kv.page_elems(layer, pg, kvh, 0) + key_elem(sl, c, D)];
     s_v[d][c] = kv.kv[kv.page_elems(layer, pg, kvh, 1) + (int64_t)c * P + sl];
   }
   __syncthreads();
@@ -326,7 +326,7 @@ __global__ void __launch_bounds__(256) k_kv_compact(KvGeom kv, StepMeta meta, co
     const int d = e / D, c = e % D;
     const int dp = ctx + d + 1;
     const int pg = trow[dp / P], sl = dp % P;
-    kv.kv[kv.page_elems(layer, pg, kvh, 0) + (int64_t)sl * D + c] = s_k[d][c];
+    kv.kv[kv.page_elems(layer, pg, kvh, 0) + key_elem(sl, c, D)] = s_k[d][c];
     kv.kv[kv.page_elems(layer, pg, kvh, 1) + (int64_t)c * P + sl] = s_v[d][c];
   }
 }

@@ -167,12 +167,25 @@ class Pool:
         c = self.cfg
         return self.kv.view(c.n_layers, self.num_pages, c.n_kv_heads, 2, c.page_size, c.head_dim)
 
+    def _key_order(self) -> torch.Tensor:
+        """Element index, inside a page's K region, of key slot s and dim d
+        ([P, D]): the fragment order of include/war.h (groups of eight slots
+        by (s / 4) % 2, 32-dim k-steps, eight 64-byte rows per run)."""
+        c = self.cfg
+        s = torch.arange(c.page_size).view(-1, 1)
+        d = torch.arange(c.head_dim).view(1, -1)
+        t, s8 = (s // 4) % 2, (s // 8) * 4 + s % 4
+        return ((t * (c.head_dim // 32) + d // 32) * 8 + s8) * 32 + d % 32
+
     def gather_kv(self, seq: int, n_tokens: int, layer: int) -> torch.Tensor:
         """[2, Hkv, n_tokens, D] keys/values of a sequence read back from its pages."""
         c = self.cfg
         pages = self.block_tables[seq, : -(-n_tokens // c.page_size)].long()
         v = self.kv_view()[layer, pages]                       # [np, H, 2, P, D]
-        k = v[:, :, 0].permute(1, 0, 2, 3).reshape(c.n_kv_heads, -1, c.head_dim)
+        kraw = v[:, :, 0].reshape(len(pages), c.n_kv_heads, c.page_size * c.head_dim)
+        korder = self._key_order().to(kraw.device).reshape(-1)
+        k = kraw[:, :, korder].reshape(len(pages), c.n_kv_heads, c.page_size, c.head_dim)
+        k = k.permute(1, 0, 2, 3).reshape(c.n_kv_heads, -1, c.head_dim)
         vt = v[:, :, 1].reshape(len(pages), c.n_kv_heads, c.head_dim, c.page_size)
         vv = vt.permute(1, 0, 3, 2).reshape(c.n_kv_heads, -1, c.head_dim)
         return torch.stack([k[:, :n_tokens], vv[:, :n_tokens]])
